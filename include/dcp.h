@@ -1,0 +1,263 @@
+/*
+ * dcp.h -- C ABI of the Data-Centric Parallel (DCP) hot path on one MI355X.
+ *
+ * Four operations, named after the quantities of the paper's problem
+ * statement (Sec. 3.2: n batches with variable sequence lengths s_i, one
+ * configuration chosen per batch):
+ *
+ *   dcp_varlen_attn_fwd  exact softmax attention over packed variable-length
+ *                        sequences (block diagonal), returning O and the
+ *                        natural-log row log-sum-exp;
+ *   dcp_varlen_attn_bwd  its gradients dQ, dK, dV for an upstream dO;
+ *   dcp_profile_cost     measured per-length attention cost rows (the
+ *                        profiling step of Sec. 3.5);
+ *   dcp_plan             per-batch sequence-parallel size, micro-batch,
+ *                        gradient accumulation and recomputed layers
+ *                        (DCP-intra, Sec. 3.4 / Algorithm 1; DCP-inter,
+ *                        Sec. 3.3 / Eq. (3) / Appendix C).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Status: every call returns 0 (DCP_OK) or a negative dcp_status and never
+ *   throws across the ABI.  dcp_last_error() returns a thread-local message
+ *   for the last failing call on the calling thread.
+ * - Ownership: the caller owns every buffer.  The library never allocates
+ *   device memory: scratch space comes from a caller-provided workspace whose
+ *   size is queried first.  Host arrays are read only during the call.
+ * - Streams: `stream` is a hipStream_t passed as void* (NULL = the null
+ *   stream).  Attention calls enqueue work and return without synchronising;
+ *   argument errors are detected on the host before anything is enqueued;
+ *   a launch failure is reported as DCP_ERR_HIP, while execution faults
+ *   surface at the caller's next synchronisation.  dcp_profile_cost
+ *   synchronises.  dcp_plan touches no device.
+ * - Layout: Q, K, V, O, dO, dQ, dK, dV are bf16 [T, H, D] row-major (token
+ *   stride H*D, head stride D, D contiguous), device memory, 16-byte aligned.
+ *   LSE is fp32 [H, T].  Rows beyond cu_seqlens[n_seqs] are neither read
+ *   for any output nor written.
+ */
+#ifndef DCP_H
+#define DCP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DCP_OK = 0,
+  DCP_ERR_INVALID = -1,     /* bad argument (null, inconsistent sizes, overflow) */
+  DCP_ERR_UNSUPPORTED = -2, /* valid but not implemented (e.g. head_dim) */
+  DCP_ERR_HIP = -3,         /* HIP runtime error, or no usable gfx950 device */
+  DCP_ERR_WORKSPACE = -4,   /* workspace null or smaller than queried */
+  DCP_ERR_INFEASIBLE = -5,  /* planner: no configuration fits the memory budget */
+  DCP_ERR_TABLE = -6        /* planner: bad cost table or length beyond it */
+} dcp_status;
+
+/* Message for the last failing call on this thread ("" if none). */
+const char* dcp_last_error(void);
+
+/* Library version string. */
+const char* dcp_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* Packed variable-length attention                                          */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Describes one packed batch.  Sequence b owns token rows
+ * cu_seqlens_host[b] .. cu_seqlens_host[b+1]-1 and attends only to itself
+ * (the "packed parallel" layout of Sec. 1; attention itself is exact softmax
+ * attention, Sec. 4.1).
+ *   n_seqs          >= 1; empty sequences (equal neighbours) are allowed.
+ *   cu_seqlens_host host int32 [n_seqs+1]: cu[0] = 0, non-decreasing,
+ *                   cu[n_seqs] <= total_tokens.
+ *   total_tokens    T, rows allocated in every [T, H, D] tensor, < 2^31.
+ *   n_heads         H >= 1 (all heads share cu_seqlens).
+ *   head_dim        D in {64, 72, 128}; anything else is DCP_ERR_UNSUPPORTED.
+ *   scale           softmax scale applied to Q K^T, finite and > 0
+ *                   (1/sqrt(D) in the usual models).
+ *   causal          0: every query sees its whole sequence;
+ *                   1: query i sees keys j <= i of its sequence.
+ */
+typedef struct {
+  int32_t n_seqs;
+  const int32_t* cu_seqlens_host;
+  int64_t total_tokens;
+  int32_t n_heads;
+  int32_t head_dim;
+  float scale;
+  int32_t causal;
+} dcp_attn_desc;
+
+/* Workspace bytes needed by dcp_varlen_attn_fwd / _bwd for this batch. */
+int dcp_varlen_attn_fwd_workspace_size(const dcp_attn_desc* desc, size_t* bytes);
+int dcp_varlen_attn_bwd_workspace_size(const dcp_attn_desc* desc, size_t* bytes);
+
+/*
+ * Forward: for each sequence and head, O = softmax(scale * Q K^T) V and
+ * LSE = ln sum_j exp(scale * q_i . k_j) (fp32, natural log), computed with
+ * bf16 matrix-core products, fp32 accumulation and an fp32 online softmax.
+ *   q, k, v    bf16 [T, H, D] inputs.
+ *   o          bf16 [T, H, D] output (rows of sequences only).
+ *   lse        fp32 [H, T] output (rows of sequences only).
+ *   workspace  device scratch of at least the queried size.
+ */
+int dcp_varlen_attn_fwd(const dcp_attn_desc* desc, const void* q, const void* k, const void* v,
+                        void* o, float* lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Backward of the forward above for the loss <dO, O>:
+ *   dV = P^T dO,  dS = P o (dO V^T - rowsum(dO o O)),
+ *   dQ = scale dS K,  dK = scale dS^T Q,  with P = exp(scale Q K^T - LSE).
+ *   dout, o, lse  the upstream gradient and the forward's O and LSE.
+ *   q, k, v       the forward's inputs.
+ *   dq, dk, dv    bf16 [T, H, D] outputs (rows of sequences only).
+ *   workspace     device scratch of at least the queried size; it holds the
+ *                 fp32 dQ accumulator and rowsum(dO o O).
+ * The call uses the same desc (scale, causal) as the forward.
+ */
+int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, const void* o, const float* lse,
+                        const void* q, const void* k, const void* v, void* dq, void* dk, void* dv,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Per-length cost profile (Sec. 3.5)                                        */
+/* ------------------------------------------------------------------------ */
+
+/* One profile row: per-layer costs of one sequence of length seq_len with
+ * micro-batch 1 on one device. */
+typedef struct {
+  int64_t seq_len;
+  int64_t t_f_ns;      /* forward time of one layer */
+  int64_t t_b_ns;      /* backward time of one layer (no recompute) */
+  int64_t m_bytes;     /* activations one layer stashes for backward */
+  int64_t m_inp_bytes; /* the layer's input activation */
+} dcp_cost_row;
+
+/*
+ * Profiling options.  Times are the median over `reps` timed runs after
+ * `warmup` untimed ones (the paper times the second of two layers, the
+ * first being warm-up).  lin_*_ps_per_token add a caller-supplied linear
+ * per-token term (picoseconds/token) for the non-attention part of a layer.
+ * Memory is analytic: m = s * act_bytes_per_token, m_inp = s *
+ * inp_bytes_per_token.  scale <= 0 selects 1/sqrt(head_dim).
+ */
+typedef struct {
+  int32_t n_heads;
+  int32_t head_dim;
+  int32_t causal;
+  float scale;
+  int32_t warmup;
+  int32_t reps;
+  int64_t lin_f_ps_per_token;
+  int64_t lin_b_ps_per_token;
+  int64_t act_bytes_per_token;
+  int64_t inp_bytes_per_token;
+} dcp_profile_opts;
+
+/* Workspace bytes for profiling lengths up to max_len. */
+int dcp_profile_workspace_size(int64_t max_len, const dcp_profile_opts* opts, size_t* bytes);
+
+/*
+ * Measure one row per length: a single sequence of lengths[i] tokens with
+ * the given heads and width, synthetic inputs written into the workspace,
+ * forward and backward timed with HIP events on `stream`.  Synchronises.
+ *   lengths   host int64 [n], each in [1, max_len used for the workspace].
+ *   out_rows  host [n], written only on success.
+ */
+int dcp_profile_cost(const int64_t* lengths, int32_t n, const dcp_profile_opts* opts, void* workspace,
+                     size_t workspace_bytes, void* stream, dcp_cost_row* out_rows);
+
+/* ------------------------------------------------------------------------ */
+/* Planner (Secs. 3.2-3.5, Appendix C)                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Cost table: rows strictly increasing in seq_len, every value >= 0, plus
+ * the model constants of Eqs. (4)-(6): layer count L, constant time T_C and
+ * constant memory M_C. */
+typedef struct {
+  const dcp_cost_row* rows;
+  int32_t n_rows;
+  int32_t n_layers;
+  int64_t T_C_ns;
+  int64_t M_C_bytes;
+} dcp_cost_table;
+
+enum {
+  DCP_PLAN_INTER = 0, /* DCP-inter: full recomputation, balance by accumulation */
+  DCP_PLAN_INTRA = 1  /* DCP-intra: fewest recomputed layers that fit memory */
+};
+enum {
+  DCP_PLAN_FLAG_MIN_TIME = 1,      /* rank candidates by raw step time, not Eq. (1) throughput */
+  DCP_PLAN_FLAG_NO_HEAD_FILTER = 2 /* allow p that does not divide n_heads */
+};
+
+/*
+ * Planner options (NULL = defaults from dcp_plan_opts_default):
+ *   sp_cands/n_sp       candidate sequence-parallel sizes, strictly increasing
+ *                       (default {1,2,4,8}).
+ *   b_max               micro-batch sizes 1..b_max are tried (default 64).
+ *   n_heads             head count; p must divide it (default 16).
+ *   hidden              hidden size moved by each Ulysses all-to-all (1152).
+ *   a2a_alpha_ns        per-all-to-all latency (10000).
+ *   link_bytes_per_ns   bytes per ns of one point-to-point link (153).
+ *   g_min, g_max        accumulation bounds of Appendix C (1, 4).
+ *   mode                DCP_PLAN_INTRA (default) or DCP_PLAN_INTER.
+ *   flags               DCP_PLAN_FLAG_* bits (0).
+ */
+typedef struct {
+  const int32_t* sp_cands;
+  int32_t n_sp;
+  int32_t b_max;
+  int32_t n_heads;
+  int64_t hidden;
+  int64_t a2a_alpha_ns;
+  int64_t link_bytes_per_ns;
+  int32_t g_min;
+  int32_t g_max;
+  int32_t mode;
+  int32_t flags;
+} dcp_plan_opts;
+
+void dcp_plan_opts_default(dcp_plan_opts* opts);
+
+/* Caller-sized outputs, one entry per batch; recompute_flags holds
+ * n_batches * n_layers bytes, flag [i*L + l] = 1 iff layer l of batch i is
+ * recomputed (the first r_i layers).  step_time_ns and mem_bytes may be NULL.
+ * idle_ns and makespan_ns describe the whole iteration: makespan =
+ * max_i g_i*T_i and idle = sum_i (makespan - g_i*T_i) (Eq. (3) times W). */
+typedef struct {
+  int32_t* sp_size;
+  int32_t* micro_batch;
+  int32_t* grad_accum;
+  int32_t* recompute_layers;
+  uint8_t* recompute_flags;
+  int64_t* step_time_ns;
+  int64_t* mem_bytes;
+  int64_t idle_ns;
+  int64_t makespan_ns;
+} dcp_plan_out;
+
+/*
+ * Plan one iteration.  Every sequence is its own batch when batch_offsets
+ * is NULL (then n_batches must equal n_seqs); otherwise batch i packs
+ * sequences batch_offsets[i] .. batch_offsets[i+1]-1 (CSR, n_batches+1
+ * entries, each batch non-empty).  Each sequence takes the table row with
+ * the smallest length >= its own; a pack sums its rows.  All arithmetic is
+ * int64 with overflow checks (DCP_ERR_INVALID); the result is bit-exact
+ * and deterministic.  Outputs are written only on success.
+ * Errors: DCP_ERR_INVALID (arguments), DCP_ERR_TABLE (table or a length
+ * beyond it), DCP_ERR_INFEASIBLE (no (p, b, r) fits hbm_budget_bytes; the
+ * message names the batch).
+ */
+int dcp_plan(const int64_t* seq_lens, int32_t n_seqs, const int32_t* batch_offsets, int32_t n_batches,
+             const dcp_cost_table* table, int64_t hbm_budget_bytes, const dcp_plan_opts* opts,
+             dcp_plan_out* out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DCP_H */

@@ -277,9 +277,10 @@ def _choose_config(u: _Unit, table: CostTable, budget: int, o: PlanOpts, batch_i
             else:
                 # Algorithm 1: the smallest number of recomputed layers whose
                 # stashed activations still fit, Eq. (6).
+                # (exact integers: an unrepresentable total simply does not fit)
                 r = None
                 for rr in range(0, L + 1):
-                    if _fit(_fit((L - rr) * c.m) + c.M_bp) <= budget:
+                    if (L - rr) * c.m + c.M_bp <= budget:
                         r = rr
                         break
                 assert r is not None  # rr = L always fits once M_bp <= budget
@@ -355,6 +356,8 @@ def plan(seq_lens: Sequence[int], table: CostTable, hbm_budget: int, opts: Optio
     if min(out.step_time_ns) == 0:
         raise PlanError(ERR_TABLE, "a batch has zero step time; the cost table is empty of cost")
     g, idle, span = accumulation_steps(out.step_time_ns, o.g_min, o.g_max)
+    if max(g) > (1 << 31) - 1:
+        raise PlanError(ERR_INVALID, "accumulation steps exceed int32")
     out.grad_accum = g
     out.idle_ns = idle
     out.makespan_ns = span

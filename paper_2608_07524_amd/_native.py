@@ -1,0 +1,337 @@
+"""ctypes binding of libdcp (the C ABI in include/dcp.h).
+
+Argument marshalling only: every step of attention, profiling and planning
+runs inside libdcp.  PyTorch supplies device memory and the current stream.
+The library must be built (``python -m paper_2608_07524_amd.build``); there
+is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import math
+import os
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdcp.so")
+
+DCP_OK = 0
+DCP_ERR_INVALID = -1
+DCP_ERR_UNSUPPORTED = -2
+DCP_ERR_HIP = -3
+DCP_ERR_WORKSPACE = -4
+DCP_ERR_INFEASIBLE = -5
+DCP_ERR_TABLE = -6
+
+PLAN_INTER = 0
+PLAN_INTRA = 1
+PLAN_FLAG_MIN_TIME = 1
+PLAN_FLAG_NO_HEAD_FILTER = 2
+
+
+class DCPError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libdcp error {code}: {msg}")
+        self.code = code
+
+
+class AttnDesc(C.Structure):
+    _fields_ = [("n_seqs", C.c_int32), ("cu_seqlens_host", C.POINTER(C.c_int32)), ("total_tokens", C.c_int64),
+                ("n_heads", C.c_int32), ("head_dim", C.c_int32), ("scale", C.c_float), ("causal", C.c_int32)]
+
+
+class CostRow(C.Structure):
+    _fields_ = [("seq_len", C.c_int64), ("t_f_ns", C.c_int64), ("t_b_ns", C.c_int64), ("m_bytes", C.c_int64),
+                ("m_inp_bytes", C.c_int64)]
+
+
+class ProfileOpts(C.Structure):
+    _fields_ = [("n_heads", C.c_int32), ("head_dim", C.c_int32), ("causal", C.c_int32), ("scale", C.c_float),
+                ("warmup", C.c_int32), ("reps", C.c_int32), ("lin_f_ps_per_token", C.c_int64),
+                ("lin_b_ps_per_token", C.c_int64), ("act_bytes_per_token", C.c_int64),
+                ("inp_bytes_per_token", C.c_int64)]
+
+
+class CostTableC(C.Structure):
+    _fields_ = [("rows", C.POINTER(CostRow)), ("n_rows", C.c_int32), ("n_layers", C.c_int32),
+                ("T_C_ns", C.c_int64), ("M_C_bytes", C.c_int64)]
+
+
+class PlanOptsC(C.Structure):
+    _fields_ = [("sp_cands", C.POINTER(C.c_int32)), ("n_sp", C.c_int32), ("b_max", C.c_int32),
+                ("n_heads", C.c_int32), ("hidden", C.c_int64), ("a2a_alpha_ns", C.c_int64),
+                ("link_bytes_per_ns", C.c_int64), ("g_min", C.c_int32), ("g_max", C.c_int32),
+                ("mode", C.c_int32), ("flags", C.c_int32)]
+
+
+class PlanOutC(C.Structure):
+    _fields_ = [("sp_size", C.POINTER(C.c_int32)), ("micro_batch", C.POINTER(C.c_int32)),
+                ("grad_accum", C.POINTER(C.c_int32)), ("recompute_layers", C.POINTER(C.c_int32)),
+                ("recompute_flags", C.POINTER(C.c_uint8)), ("step_time_ns", C.POINTER(C.c_int64)),
+                ("mem_bytes", C.POINTER(C.c_int64)), ("idle_ns", C.c_int64), ("makespan_ns", C.c_int64)]
+
+
+_lib = None
+
+
+def load() -> C.CDLL:
+    """Load libdcp.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_07524_amd.build`")
+    lib = C.CDLL(LIB_PATH)
+    vp, sz = C.c_void_p, C.c_size_t
+    sig = {
+        "dcp_last_error": ([], C.c_char_p),
+        "dcp_version": ([], C.c_char_p),
+        "dcp_varlen_attn_fwd_workspace_size": ([C.POINTER(AttnDesc), C.POINTER(sz)], C.c_int),
+        "dcp_varlen_attn_bwd_workspace_size": ([C.POINTER(AttnDesc), C.POINTER(sz)], C.c_int),
+        "dcp_varlen_attn_fwd": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp, sz, vp], C.c_int),
+        "dcp_varlen_attn_bwd": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], C.c_int),
+        "dcp_profile_workspace_size": ([C.c_int64, C.POINTER(ProfileOpts), C.POINTER(sz)], C.c_int),
+        "dcp_profile_cost": ([C.POINTER(C.c_int64), C.c_int32, C.POINTER(ProfileOpts), vp, sz, vp,
+                              C.POINTER(CostRow)], C.c_int),
+        "dcp_plan_opts_default": ([C.POINTER(PlanOptsC)], None),
+        "dcp_plan": ([C.POINTER(C.c_int64), C.c_int32, C.POINTER(C.c_int32), C.c_int32, C.POINTER(CostTableC),
+                      C.c_int64, C.POINTER(PlanOptsC), C.POINTER(PlanOutC)], C.c_int),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def last_error() -> str:
+    return load().dcp_last_error().decode()
+
+
+def _check(status: int):
+    if status != DCP_OK:
+        raise DCPError(status, last_error())
+
+
+# ---------------------------------------------------------------------------
+# attention
+
+class _Desc:
+    """Keeps a dcp_attn_desc and the host cu_seqlens array it points to alive."""
+
+    def __init__(self, cu_seqlens, total_tokens: int, n_heads: int, head_dim: int, scale: float, causal: bool):
+        self.cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+        self.desc = AttnDesc(int(self.cu.size - 1), self.cu.ctypes.data_as(C.POINTER(C.c_int32)), int(total_tokens),
+                             int(n_heads), int(head_dim), float(scale), int(bool(causal)))
+
+    @property
+    def ref(self):
+        return C.byref(self.desc)
+
+
+def _host_cu(cu_seqlens):
+    if hasattr(cu_seqlens, "detach"):
+        cu_seqlens = cu_seqlens.detach().cpu().numpy()
+    return np.asarray(cu_seqlens, dtype=np.int32)
+
+
+def _stream_ptr(torch, device):
+    return C.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def fwd_workspace_size(cu_seqlens, total_tokens, n_heads, head_dim, scale=1.0, causal=False) -> int:
+    d = _Desc(_host_cu(cu_seqlens), total_tokens, n_heads, head_dim, scale, causal)
+    n = C.c_size_t()
+    _check(load().dcp_varlen_attn_fwd_workspace_size(d.ref, C.byref(n)))
+    return n.value
+
+
+def bwd_workspace_size(cu_seqlens, total_tokens, n_heads, head_dim, scale=1.0, causal=False) -> int:
+    d = _Desc(_host_cu(cu_seqlens), total_tokens, n_heads, head_dim, scale, causal)
+    n = C.c_size_t()
+    _check(load().dcp_varlen_attn_bwd_workspace_size(d.ref, C.byref(n)))
+    return n.value
+
+
+def _check_qkv(torch, *ts):
+    for t in ts:
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() or t.dim() != 3:
+            raise ValueError("tensors must be contiguous bf16 CUDA tensors of shape [T, H, D]")
+
+
+def varlen_attn_fwd(q, k, v, cu_seqlens, scale: Optional[float] = None, causal: bool = False,
+                    out=None, lse=None, workspace=None):
+    """O, LSE = attention over packed sequences (see dcp_varlen_attn_fwd)."""
+    import torch
+    _check_qkv(torch, q, k, v)
+    T, H, D = q.shape
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    d = _Desc(_host_cu(cu_seqlens), T, H, D, scale, causal)
+    lib = load()
+    n = C.c_size_t()
+    _check(lib.dcp_varlen_attn_fwd_workspace_size(d.ref, C.byref(n)))
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty((H, T), dtype=torch.float32, device=q.device) if lse is None else lse
+    ws = torch.empty(n.value, dtype=torch.uint8, device=q.device) if workspace is None else workspace
+    _check(lib.dcp_varlen_attn_fwd(d.ref, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                                   ws.data_ptr(), ws.numel(), _stream_ptr(torch, q.device)))
+    return o, lse
+
+
+def varlen_attn_bwd(dout, o, lse, q, k, v, cu_seqlens, scale: Optional[float] = None, causal: bool = False,
+                    dq=None, dk=None, dv=None, workspace=None):
+    """dQ, dK, dV of the loss <dO, O> (see dcp_varlen_attn_bwd)."""
+    import torch
+    _check_qkv(torch, dout, o, q, k, v)
+    T, H, D = q.shape
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    d = _Desc(_host_cu(cu_seqlens), T, H, D, scale, causal)
+    lib = load()
+    n = C.c_size_t()
+    _check(lib.dcp_varlen_attn_bwd_workspace_size(d.ref, C.byref(n)))
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    ws = torch.empty(n.value, dtype=torch.uint8, device=q.device) if workspace is None else workspace
+    _check(lib.dcp_varlen_attn_bwd(d.ref, dout.data_ptr(), o.data_ptr(), lse.data_ptr(), q.data_ptr(),
+                                   k.data_ptr(), v.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                                   ws.data_ptr(), ws.numel(), _stream_ptr(torch, q.device)))
+    return dq, dk, dv
+
+
+class PreparedAttention:
+    """Pre-marshalled forward + backward calls on fixed buffers.
+
+    Builds the descriptor and workspaces once so repeated calls (benchmarks,
+    training loops over the same packed batch) pay only the C call.
+    """
+
+    def __init__(self, q, k, v, dout, cu_seqlens, scale: Optional[float] = None, causal: bool = False):
+        import torch
+        _check_qkv(torch, q, k, v, dout)
+        self.torch = torch
+        T, H, D = q.shape
+        self.scale = 1.0 / math.sqrt(D) if scale is None else scale
+        self.d = _Desc(_host_cu(cu_seqlens), T, H, D, self.scale, causal)
+        lib = self.lib = load()
+        n1, n2 = C.c_size_t(), C.c_size_t()
+        _check(lib.dcp_varlen_attn_fwd_workspace_size(self.d.ref, C.byref(n1)))
+        _check(lib.dcp_varlen_attn_bwd_workspace_size(self.d.ref, C.byref(n2)))
+        self.q, self.k, self.v, self.dout = q, k, v, dout
+        self.o = torch.empty_like(q)
+        self.lse = torch.empty((H, T), dtype=torch.float32, device=q.device)
+        self.dq, self.dk, self.dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+        self.ws_f = torch.empty(max(1, n1.value), dtype=torch.uint8, device=q.device)
+        self.ws_b = torch.empty(max(1, n2.value), dtype=torch.uint8, device=q.device)
+        self.stream = _stream_ptr(torch, q.device)
+
+    def fwd(self):
+        _check(self.lib.dcp_varlen_attn_fwd(self.d.ref, self.q.data_ptr(), self.k.data_ptr(), self.v.data_ptr(),
+                                            self.o.data_ptr(), self.lse.data_ptr(), self.ws_f.data_ptr(),
+                                            self.ws_f.numel(), self.stream))
+
+    def bwd(self):
+        _check(self.lib.dcp_varlen_attn_bwd(self.d.ref, self.dout.data_ptr(), self.o.data_ptr(),
+                                            self.lse.data_ptr(), self.q.data_ptr(), self.k.data_ptr(),
+                                            self.v.data_ptr(), self.dq.data_ptr(), self.dk.data_ptr(),
+                                            self.dv.data_ptr(), self.ws_b.data_ptr(), self.ws_b.numel(),
+                                            self.stream))
+
+    def step(self):
+        self.fwd()
+        self.bwd()
+
+
+# ---------------------------------------------------------------------------
+# profiling
+
+def profile_cost(lengths: Sequence[int], n_heads: int, head_dim: int, causal: bool = False,
+                 scale: float = 0.0, warmup: int = 3, reps: int = 10, lin_f_ps_per_token: int = 0,
+                 lin_b_ps_per_token: int = 0, act_bytes_per_token: int = 0, inp_bytes_per_token: int = 0,
+                 device=None) -> List[CostRow]:
+    """Measured per-length cost rows (see dcp_profile_cost)."""
+    import torch
+    lib = load()
+    opts = ProfileOpts(n_heads, head_dim, int(causal), scale, warmup, reps, lin_f_ps_per_token,
+                       lin_b_ps_per_token, act_bytes_per_token, inp_bytes_per_token)
+    lens = np.ascontiguousarray(np.asarray(lengths, dtype=np.int64))
+    n = C.c_size_t()
+    _check(lib.dcp_profile_workspace_size(int(lens.max()), C.byref(opts), C.byref(n)))
+    dev = torch.device("cuda") if device is None else device
+    ws = torch.empty(n.value, dtype=torch.uint8, device=dev)
+    out = (CostRow * lens.size)()
+    _check(lib.dcp_profile_cost(lens.ctypes.data_as(C.POINTER(C.c_int64)), int(lens.size), C.byref(opts),
+                                ws.data_ptr(), ws.numel(), _stream_ptr(torch, dev), out))
+    return [CostRow(r.seq_len, r.t_f_ns, r.t_b_ns, r.m_bytes, r.m_inp_bytes) for r in out]
+
+
+# ---------------------------------------------------------------------------
+# planner
+
+@dataclass
+class Plan:
+    sp_size: List[int] = field(default_factory=list)
+    micro_batch: List[int] = field(default_factory=list)
+    grad_accum: List[int] = field(default_factory=list)
+    recompute_layers: List[int] = field(default_factory=list)
+    recompute_flags: List[int] = field(default_factory=list)
+    step_time_ns: List[int] = field(default_factory=list)
+    mem_bytes: List[int] = field(default_factory=list)
+    idle_ns: int = 0
+    makespan_ns: int = 0
+
+
+def default_plan_opts() -> dict:
+    o = PlanOptsC()
+    load().dcp_plan_opts_default(C.byref(o))
+    return dict(sp_cands=tuple(o.sp_cands[i] for i in range(o.n_sp)), b_max=o.b_max, n_heads=o.n_heads,
+                hidden=o.hidden, a2a_alpha_ns=o.a2a_alpha_ns, link_bytes_per_ns=o.link_bytes_per_ns,
+                g_min=o.g_min, g_max=o.g_max, mode=o.mode, flags=o.flags)
+
+
+def plan(seq_lens: Sequence[int], rows: Sequence, n_layers: int, T_C_ns: int, M_C_bytes: int, hbm_budget: int,
+         batch_offsets: Optional[Sequence[int]] = None, n_batches: Optional[int] = None, **opts) -> Plan:
+    """Plan one iteration (see dcp_plan).  ``rows``: (seq_len, t_f, t_b, m, m_inp)
+    tuples or CostRow objects; ``opts`` override dcp_plan_opts_default."""
+    lib = load()
+    o = PlanOptsC()
+    lib.dcp_plan_opts_default(C.byref(o))
+    sp = None
+    for key, val in opts.items():
+        if key == "sp_cands":
+            sp = np.ascontiguousarray(np.asarray(val, dtype=np.int32))
+            o.sp_cands = sp.ctypes.data_as(C.POINTER(C.c_int32))
+            o.n_sp = int(sp.size)
+        elif hasattr(o, key):
+            setattr(o, key, int(val))
+        else:
+            raise TypeError(f"unknown planner option {key}")
+    crow = (CostRow * len(rows))()
+    for i, r in enumerate(rows):
+        vals = (r.seq_len, r.t_f_ns, r.t_b_ns, r.m_bytes, r.m_inp_bytes) if hasattr(r, "seq_len") else tuple(r)
+        crow[i] = CostRow(*[int(x) for x in vals])
+    table = CostTableC(crow, len(rows), int(n_layers), int(T_C_ns), int(M_C_bytes))
+    lens = np.ascontiguousarray(np.asarray(seq_lens, dtype=np.int64))
+    offs = None
+    if batch_offsets is not None:
+        offs = np.ascontiguousarray(np.asarray(batch_offsets, dtype=np.int32))
+        nb = int(offs.size - 1) if n_batches is None else int(n_batches)
+    else:
+        nb = int(lens.size) if n_batches is None else int(n_batches)
+    nb_alloc = max(nb, 1)
+    i32 = lambda: (C.c_int32 * nb_alloc)()
+    i64 = lambda: (C.c_int64 * nb_alloc)()
+    sp_o, mb_o, ga_o, rl_o = i32(), i32(), i32(), i32()
+    fl_o = (C.c_uint8 * max(1, nb_alloc * max(1, int(n_layers))))()
+    st_o, mem_o = i64(), i64()
+    out = PlanOutC(sp_o, mb_o, ga_o, rl_o, fl_o, st_o, mem_o, 0, 0)
+    _check(lib.dcp_plan(lens.ctypes.data_as(C.POINTER(C.c_int64)), int(lens.size),
+                        None if offs is None else offs.ctypes.data_as(C.POINTER(C.c_int32)), nb, C.byref(table),
+                        int(hbm_budget), C.byref(o), C.byref(out)))
+    L = int(n_layers)
+    return Plan(list(sp_o[:nb]), list(mb_o[:nb]), list(ga_o[:nb]), list(rl_o[:nb]), list(fl_o[:nb * L]),
+                list(st_o[:nb]), list(mem_o[:nb]), out.idle_ns, out.makespan_ns)

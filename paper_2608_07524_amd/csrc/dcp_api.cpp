@@ -1,0 +1,362 @@
+// C ABI of libdcp: argument validation, work lists, workspace layout,
+// kernel launches and the per-length cost profiler.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "attn_common.h"
+#include "attn_launch.h"
+#include "dcp_internal.h"
+
+namespace dcp {
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// The kernels are built for gfx950 only; refuse other devices up front.
+int check_device() {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "no HIP device: %s", hipGetErrorString(e));
+  static std::mutex mu;
+  static std::vector<int> ok_devices;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    if (std::find(ok_devices.begin(), ok_devices.end(), dev) != ok_devices.end()) return DCP_OK;
+  }
+  hipDeviceProp_t prop;
+  e = hipGetDeviceProperties(&prop, dev);
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(DCP_ERR_HIP, "device %d is %s; libdcp is built for gfx950 only", dev, prop.gcnArchName);
+  std::lock_guard<std::mutex> lock(mu);
+  ok_devices.push_back(dev);
+  return DCP_OK;
+}
+
+int validate_desc(const dcp_attn_desc* d) {
+  if (!d) return fail(DCP_ERR_INVALID, "desc is null");
+  if (d->n_seqs < 1) return fail(DCP_ERR_INVALID, "n_seqs must be >= 1");
+  if (!d->cu_seqlens_host) return fail(DCP_ERR_INVALID, "cu_seqlens_host is null");
+  if (d->total_tokens < 0 || d->total_tokens >= (int64_t(1) << 31))
+    return fail(DCP_ERR_INVALID, "total_tokens must be in [0, 2^31)");
+  if (d->n_heads < 1) return fail(DCP_ERR_INVALID, "n_heads must be >= 1");
+  if (d->head_dim != 64 && d->head_dim != 72 && d->head_dim != 128)
+    return fail(DCP_ERR_UNSUPPORTED, "head_dim %d is not supported (64, 72, 128)", d->head_dim);
+  if (!(std::isfinite(d->scale) && d->scale > 0.f)) return fail(DCP_ERR_INVALID, "scale must be finite and > 0");
+  if (d->causal != 0 && d->causal != 1) return fail(DCP_ERR_INVALID, "causal must be 0 or 1");
+  const int32_t* cu = d->cu_seqlens_host;
+  if (cu[0] != 0) return fail(DCP_ERR_INVALID, "cu_seqlens[0] must be 0");
+  for (int32_t b = 0; b < d->n_seqs; ++b)
+    if (cu[b + 1] < cu[b]) return fail(DCP_ERR_INVALID, "cu_seqlens must be non-decreasing (index %d)", b + 1);
+  if (cu[d->n_seqs] > d->total_tokens)
+    return fail(DCP_ERR_INVALID, "cu_seqlens[n] = %d exceeds total_tokens", cu[d->n_seqs]);
+  const int64_t elems = d->total_tokens * int64_t(d->n_heads) * d->head_dim;
+  if (elems / d->n_heads / d->head_dim != d->total_tokens) return fail(DCP_ERR_INVALID, "tensor size overflows");
+  return DCP_OK;
+}
+
+int check_tensor(const void* p, const char* name) {
+  if (!p) return fail(DCP_ERR_INVALID, "%s is null", name);
+  if (reinterpret_cast<uintptr_t>(p) % 16 != 0) return fail(DCP_ERR_INVALID, "%s must be 16-byte aligned", name);
+  return DCP_OK;
+}
+
+// Tiles of `tile` rows per sequence, never straddling two sequences, in
+// longest-processing-time-first order (work of a tile: the keys it visits
+// in the forward, or the queries it visits in the backward).
+std::vector<WorkUnit> build_units(const dcp_attn_desc* d, int tile, bool keys_major) {
+  std::vector<WorkUnit> units;
+  std::vector<int64_t> work;
+  const int32_t* cu = d->cu_seqlens_host;
+  for (int32_t b = 0; b < d->n_seqs; ++b) {
+    const int32_t s0 = cu[b], len = cu[b + 1] - cu[b];
+    for (int32_t t0 = 0; t0 < len; t0 += tile) {
+      const int32_t rows = std::min(tile, len - t0);
+      units.push_back(WorkUnit{s0 + t0, rows, s0, len});
+      int64_t w;
+      if (!d->causal) {
+        w = len;
+      } else if (!keys_major) {
+        w = int64_t(t0) + rows;  // query tile sees keys [0, t0 + rows)
+      } else {
+        w = int64_t(len) - t0;  // key tile is seen by queries [t0, len)
+      }
+      work.push_back(w);
+    }
+  }
+  std::vector<size_t> idx(units.size());
+  for (size_t i = 0; i < idx.size(); ++i) idx[i] = i;
+  std::stable_sort(idx.begin(), idx.end(), [&](size_t a, size_t b) { return work[a] > work[b]; });
+  std::vector<WorkUnit> sorted(units.size());
+  for (size_t i = 0; i < idx.size(); ++i) sorted[i] = units[idx[i]];
+  return sorted;
+}
+
+size_t count_units(const dcp_attn_desc* d, int tile) {
+  size_t n = 0;
+  for (int32_t b = 0; b < d->n_seqs; ++b)
+    n += size_t((d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b] + tile - 1) / tile);
+  return n;
+}
+
+struct BwdLayout {
+  size_t delta, dq_acc, units, total;
+};
+BwdLayout bwd_layout(const dcp_attn_desc* d) {
+  BwdLayout l;
+  const int64_t rows_end = d->cu_seqlens_host[d->n_seqs];
+  l.delta = 0;
+  l.dq_acc = align_up(size_t(4) * size_t(d->n_heads) * size_t(d->total_tokens));
+  l.units = l.dq_acc + align_up(size_t(4) * size_t(rows_end) * size_t(d->n_heads) * size_t(d->head_dim));
+  l.total = l.units + align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, kBwdBN)));
+  return l;
+}
+
+int upload_units(const std::vector<WorkUnit>& units, void* dst, hipStream_t stream) {
+  if (units.empty()) return DCP_OK;
+  hipError_t e = hipMemcpyAsync(dst, units.data(), units.size() * sizeof(WorkUnit), hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
+  return DCP_OK;
+}
+
+}  // namespace
+}  // namespace dcp
+
+using namespace dcp;
+
+extern "C" const char* dcp_last_error(void) { return g_last_error.c_str(); }
+
+extern "C" const char* dcp_version(void) { return "dcp-mi355x 0.1 (gfx950)"; }
+
+extern "C" int dcp_varlen_attn_fwd_workspace_size(const dcp_attn_desc* desc, size_t* bytes) {
+  clear_error();
+  int st = validate_desc(desc);
+  if (st) return st;
+  if (!bytes) return fail(DCP_ERR_INVALID, "bytes is null");
+  *bytes = align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(desc, fwd_tile_rows(desc->head_dim))));
+  return DCP_OK;
+}
+
+extern "C" int dcp_varlen_attn_bwd_workspace_size(const dcp_attn_desc* desc, size_t* bytes) {
+  clear_error();
+  int st = validate_desc(desc);
+  if (st) return st;
+  if (!bytes) return fail(DCP_ERR_INVALID, "bytes is null");
+  *bytes = bwd_layout(desc).total;
+  return DCP_OK;
+}
+
+extern "C" int dcp_varlen_attn_fwd(const dcp_attn_desc* desc, const void* q, const void* k, const void* v, void* o,
+                                   float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  int st = validate_desc(desc);
+  if (st) return st;
+  if ((st = check_tensor(q, "q")) || (st = check_tensor(k, "k")) || (st = check_tensor(v, "v")) ||
+      (st = check_tensor(o, "o")))
+    return st;
+  if (!lse || reinterpret_cast<uintptr_t>(lse) % 4) return fail(DCP_ERR_INVALID, "lse is null or misaligned");
+  const int tile = fwd_tile_rows(desc->head_dim);
+  const size_t need = align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(desc, tile)));
+  if (!workspace || workspace_bytes < need)
+    return fail(DCP_ERR_WORKSPACE, "forward workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(DCP_ERR_INVALID, "workspace must be 16-byte aligned");
+  if ((st = check_device())) return st;
+  const std::vector<WorkUnit> units = build_units(desc, tile, false);
+  if (units.empty()) return DCP_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = upload_units(units, workspace, s))) return st;
+  FwdArgs a{q, k, v, o, lse, workspace, int(units.size()), desc->n_heads, desc->head_dim,
+            int(desc->total_tokens), desc->scale, desc->causal, s};
+  hipError_t e = launch_fwd(a);
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "forward launch: %s", hipGetErrorString(e));
+  return DCP_OK;
+}
+
+extern "C" int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, const void* o, const float* lse,
+                                   const void* q, const void* k, const void* v, void* dq, void* dk, void* dv,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  int st = validate_desc(desc);
+  if (st) return st;
+  if ((st = check_tensor(dout, "dout")) || (st = check_tensor(o, "o")) || (st = check_tensor(q, "q")) ||
+      (st = check_tensor(k, "k")) || (st = check_tensor(v, "v")) || (st = check_tensor(dq, "dq")) ||
+      (st = check_tensor(dk, "dk")) || (st = check_tensor(dv, "dv")))
+    return st;
+  if (!lse || reinterpret_cast<uintptr_t>(lse) % 4) return fail(DCP_ERR_INVALID, "lse is null or misaligned");
+  const BwdLayout l = bwd_layout(desc);
+  if (!workspace || workspace_bytes < l.total)
+    return fail(DCP_ERR_WORKSPACE, "backward workspace needs %zu bytes, got %zu", l.total, workspace_bytes);
+  if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(DCP_ERR_INVALID, "workspace must be 16-byte aligned");
+  if ((st = check_device())) return st;
+  const std::vector<WorkUnit> units = build_units(desc, kBwdBN, true);
+  if (units.empty()) return DCP_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  if ((st = upload_units(units, ws + l.units, s))) return st;
+  BwdArgs a{dout, o, lse, q, k, v, dq, dk, dv, reinterpret_cast<float*>(ws + l.dq_acc),
+            reinterpret_cast<float*>(ws + l.delta), ws + l.units, int(units.size()),
+            desc->cu_seqlens_host[desc->n_seqs], desc->n_heads, desc->head_dim, int(desc->total_tokens),
+            desc->scale, desc->causal, s};
+  hipError_t e = launch_bwd(a);
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "backward launch: %s", hipGetErrorString(e));
+  return DCP_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Per-length cost profile.
+
+namespace {
+
+int validate_profile_opts(const dcp_profile_opts* o) {
+  if (!o) return fail(DCP_ERR_INVALID, "profile opts are null");
+  if (o->n_heads < 1) return fail(DCP_ERR_INVALID, "n_heads must be >= 1");
+  if (o->head_dim != 64 && o->head_dim != 72 && o->head_dim != 128)
+    return fail(DCP_ERR_UNSUPPORTED, "head_dim %d is not supported (64, 72, 128)", o->head_dim);
+  if (o->causal != 0 && o->causal != 1) return fail(DCP_ERR_INVALID, "causal must be 0 or 1");
+  if (!std::isfinite(o->scale)) return fail(DCP_ERR_INVALID, "scale must be finite");
+  if (o->warmup < 0 || o->reps < 1) return fail(DCP_ERR_INVALID, "need warmup >= 0 and reps >= 1");
+  if (o->lin_f_ps_per_token < 0 || o->lin_b_ps_per_token < 0 || o->act_bytes_per_token < 0 ||
+      o->inp_bytes_per_token < 0)
+    return fail(DCP_ERR_INVALID, "per-token terms must be non-negative");
+  return DCP_OK;
+}
+
+struct ProfLayout {
+  size_t tensor;  // bytes of one [max_len, H, D] bf16 tensor
+  size_t lse;
+  size_t ws_off;
+  size_t ws_bytes;
+  size_t total;
+};
+
+ProfLayout prof_layout(int64_t max_len, const dcp_profile_opts* o) {
+  ProfLayout l;
+  l.tensor = align_up(size_t(max_len) * size_t(o->n_heads) * size_t(o->head_dim) * 2);
+  l.lse = align_up(size_t(max_len) * size_t(o->n_heads) * 4);
+  int32_t cu[2] = {0, int32_t(max_len)};
+  dcp_attn_desc d{1, cu, max_len, o->n_heads, o->head_dim, 1.f, o->causal};
+  const size_t fw = align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(&d, fwd_tile_rows(o->head_dim))));
+  l.ws_bytes = std::max(fw, bwd_layout(&d).total);
+  l.ws_off = 8 * l.tensor + l.lse;
+  l.total = l.ws_off + l.ws_bytes;
+  return l;
+}
+
+}  // namespace
+
+extern "C" int dcp_profile_workspace_size(int64_t max_len, const dcp_profile_opts* opts, size_t* bytes) {
+  clear_error();
+  int st = validate_profile_opts(opts);
+  if (st) return st;
+  if (max_len < 1 || max_len >= (int64_t(1) << 31)) return fail(DCP_ERR_INVALID, "max_len must be in [1, 2^31)");
+  if (!bytes) return fail(DCP_ERR_INVALID, "bytes is null");
+  *bytes = prof_layout(max_len, opts).total;
+  return DCP_OK;
+}
+
+extern "C" int dcp_profile_cost(const int64_t* lengths, int32_t n, const dcp_profile_opts* opts, void* workspace,
+                                size_t workspace_bytes, void* stream, dcp_cost_row* out_rows) {
+  clear_error();
+  int st = validate_profile_opts(opts);
+  if (st) return st;
+  if (n < 1 || !lengths || !out_rows) return fail(DCP_ERR_INVALID, "need n >= 1 lengths and an output array");
+  int64_t max_len = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (lengths[i] < 1 || lengths[i] >= (int64_t(1) << 31))
+      return fail(DCP_ERR_INVALID, "length %lld out of range", static_cast<long long>(lengths[i]));
+    max_len = std::max(max_len, lengths[i]);
+  }
+  const ProfLayout l = prof_layout(max_len, opts);
+  if (!workspace || workspace_bytes < l.total)
+    return fail(DCP_ERR_WORKSPACE, "profile workspace needs %zu bytes for length %lld, got %zu", l.total,
+                static_cast<long long>(max_len), workspace_bytes);
+  if (reinterpret_cast<uintptr_t>(workspace) % 256) return fail(DCP_ERR_INVALID, "workspace must be 256-byte aligned");
+  if ((st = check_device())) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  void* t[8];
+  for (int i = 0; i < 8; ++i) t[i] = ws + size_t(i) * l.tensor;
+  float* lse = reinterpret_cast<float*>(ws + 8 * l.tensor);
+  void* aws = ws + l.ws_off;
+  const int64_t elems = max_len * int64_t(opts->n_heads) * opts->head_dim;
+  for (int i = 0; i < 5; ++i) {  // q, k, v, o, dO
+    hipError_t e = launch_fill_bf16(t[i], elems, 0x1234567u + 977u * uint32_t(i), s);
+    if (e != hipSuccess) return fail(DCP_ERR_HIP, "fill: %s", hipGetErrorString(e));
+  }
+  const float scale = opts->scale > 0.f ? opts->scale : 1.f / std::sqrt(float(opts->head_dim));
+  hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
+  for (auto& e : ev) {
+    if (hipEventCreate(&e) != hipSuccess) {
+      for (auto& x : ev)
+        if (x) (void)hipEventDestroy(x);
+      return fail(DCP_ERR_HIP, "hipEventCreate failed");
+    }
+  }
+  std::vector<dcp_cost_row> rows(static_cast<size_t>(n));
+  int result = DCP_OK;
+  for (int32_t i = 0; i < n && result == DCP_OK; ++i) {
+    const int64_t len = lengths[i];
+    int32_t cu[2] = {0, int32_t(len)};
+    dcp_attn_desc d{1, cu, len, opts->n_heads, opts->head_dim, scale, opts->causal};
+    std::vector<float> tf, tb;
+    for (int32_t r = 0; r < opts->warmup + opts->reps && result == DCP_OK; ++r) {
+      (void)hipEventRecord(ev[0], s);
+      result = dcp_varlen_attn_fwd(&d, t[0], t[1], t[2], t[3], lse, aws, l.ws_bytes, stream);
+      if (result) break;
+      (void)hipEventRecord(ev[1], s);
+      result = dcp_varlen_attn_bwd(&d, t[4], t[3], lse, t[0], t[1], t[2], t[5], t[6], t[7], aws, l.ws_bytes, stream);
+      if (result) break;
+      (void)hipEventRecord(ev[2], s);
+      if (hipEventSynchronize(ev[2]) != hipSuccess) {
+        result = fail(DCP_ERR_HIP, "profile run failed: %s", hipGetErrorString(hipGetLastError()));
+        break;
+      }
+      if (r >= opts->warmup) {
+        float a = 0.f, b = 0.f;
+        (void)hipEventElapsedTime(&a, ev[0], ev[1]);
+        (void)hipEventElapsedTime(&b, ev[1], ev[2]);
+        tf.push_back(a);
+        tb.push_back(b);
+      }
+    }
+    if (result) break;
+    std::sort(tf.begin(), tf.end());
+    std::sort(tb.begin(), tb.end());
+    const double mf = tf[tf.size() / 2], mb = tb[tb.size() / 2];
+    dcp_cost_row& row = rows[size_t(i)];
+    row.seq_len = len;
+    row.t_f_ns = int64_t(std::llround(mf * 1e6)) + opts->lin_f_ps_per_token * len / 1000;
+    row.t_b_ns = int64_t(std::llround(mb * 1e6)) + opts->lin_b_ps_per_token * len / 1000;
+    row.m_bytes = len * opts->act_bytes_per_token;
+    row.m_inp_bytes = len * opts->inp_bytes_per_token;
+  }
+  for (auto& e : ev) (void)hipEventDestroy(e);
+  if (result) return result;
+  std::memcpy(out_rows, rows.data(), sizeof(dcp_cost_row) * size_t(n));
+  return DCP_OK;
+}

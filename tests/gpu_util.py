@@ -1,0 +1,32 @@
+"""Helpers shared by the GPU parity tests: upload seeded bf16 inputs, run the
+HIP path through the C ABI, and compare with the float64 oracle."""
+
+from __future__ import annotations
+
+import numpy as np
+
+from paper_2608_07524_amd import inputs as I
+
+# Tolerances: outputs max-abs 1e-2, gradients max-abs relative to the
+# largest reference magnitude 2e-2 (bf16 inputs); LSE max-abs 1e-3.
+O_TOL = 1e-2
+GRAD_TOL = 2e-2
+LSE_TOL = 1e-3
+
+
+def to_device(torch, bits: np.ndarray, device="cuda"):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(device)
+
+
+def to_bits(t) -> np.ndarray:
+    import torch
+    return t.detach().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def grad_err(got_bits: np.ndarray, ref: np.ndarray) -> float:
+    got = I.bf16_to_f64(got_bits)
+    return float(np.max(np.abs(got - ref)) / max(np.max(np.abs(ref)), 1e-30))
+
+
+def max_abs(got_bits: np.ndarray, ref: np.ndarray) -> float:
+    return float(np.max(np.abs(I.bf16_to_f64(got_bits) - ref)))

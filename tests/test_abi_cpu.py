@@ -1,0 +1,98 @@
+"""The C ABI on the CPU: every declared symbol is exported, and argument
+errors are reported with the documented status before any device call."""
+
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2608_07524_amd as P
+from paper_2608_07524_amd import _native as N
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", fn)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b(dcp_[a-z0-9_]+)\s*\(", src))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = C.CDLL(N.LIB_PATH)
+    names = _declared_functions()
+    assert {"dcp_varlen_attn_fwd", "dcp_varlen_attn_bwd", "dcp_profile_cost", "dcp_plan"} <= names
+    for name in sorted(names):
+        assert hasattr(lib, name), name
+
+
+def _desc(cu, T, H=2, D=64, scale=0.125, causal=0):
+    cu = np.asarray(cu, dtype=np.int32)
+    d = N.AttnDesc(cu.size - 1, cu.ctypes.data_as(C.POINTER(C.c_int32)), T, H, D, scale, causal)
+    return d, cu
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(cu=[1, 5], T=5), N.DCP_ERR_INVALID),        # cu[0] != 0
+    (dict(cu=[0, 5, 3], T=5), N.DCP_ERR_INVALID),     # decreasing
+    (dict(cu=[0, 9], T=5), N.DCP_ERR_INVALID),        # beyond total_tokens
+    (dict(cu=[0, 5], T=5, H=0), N.DCP_ERR_INVALID),
+    (dict(cu=[0, 5], T=5, D=96), N.DCP_ERR_UNSUPPORTED),
+    (dict(cu=[0, 5], T=5, scale=0.0), N.DCP_ERR_INVALID),
+    (dict(cu=[0, 5], T=5, scale=float("nan")), N.DCP_ERR_INVALID),
+    (dict(cu=[0, 5], T=5, causal=2), N.DCP_ERR_INVALID),
+    (dict(cu=[0, 5], T=1 << 31), N.DCP_ERR_INVALID),
+])
+def test_descriptor_validation(kw, code):
+    lib = P.load()
+    d, keep = _desc(**kw)
+    n = C.c_size_t()
+    assert lib.dcp_varlen_attn_fwd_workspace_size(C.byref(d), C.byref(n)) == code
+    assert lib.dcp_varlen_attn_bwd_workspace_size(C.byref(d), C.byref(n)) == code
+    assert lib.dcp_last_error()
+
+
+def test_pointer_workspace_and_device_errors():
+    lib = P.load()
+    d, keep = _desc([0, 37, 101], 101)
+    n = C.c_size_t()
+    assert lib.dcp_varlen_attn_fwd_workspace_size(C.byref(d), C.byref(n)) == 0 and n.value > 0
+    fake = 1 << 20  # 16-byte aligned host address, never dereferenced
+    # null / misaligned tensors
+    assert lib.dcp_varlen_attn_fwd(C.byref(d), None, fake, fake, fake, fake, fake, n.value, None) == N.DCP_ERR_INVALID
+    assert lib.dcp_varlen_attn_fwd(C.byref(d), fake + 2, fake, fake, fake, fake, fake, n.value, None) \
+        == N.DCP_ERR_INVALID
+    # workspace too small
+    assert lib.dcp_varlen_attn_fwd(C.byref(d), fake, fake, fake, fake, fake, fake, n.value - 1, None) \
+        == N.DCP_ERR_WORKSPACE
+    assert "workspace" in P.last_error()
+    nb = C.c_size_t()
+    assert lib.dcp_varlen_attn_bwd_workspace_size(C.byref(d), C.byref(nb)) == 0
+    assert nb.value > 4 * 101 * 2 * 64
+    assert lib.dcp_varlen_attn_bwd(C.byref(d), *([fake] * 9), fake, nb.value - 1, None) == N.DCP_ERR_WORKSPACE
+    # valid arguments but no gfx950 device in this process
+    import torch
+    if not torch.cuda.is_available():
+        assert lib.dcp_varlen_attn_fwd(C.byref(d), fake, fake, fake, fake, fake, fake, n.value, None) \
+            == N.DCP_ERR_HIP
+
+
+def test_profile_validation():
+    lib = P.load()
+    o = N.ProfileOpts(2, 128, 0, 0.0, 1, 3, 0, 0, 0, 0)
+    n = C.c_size_t()
+    assert lib.dcp_profile_workspace_size(1024, C.byref(o), C.byref(n)) == 0 and n.value > 8 * 1024 * 2 * 128 * 2
+    bad = N.ProfileOpts(2, 80, 0, 0.0, 1, 3, 0, 0, 0, 0)
+    assert lib.dcp_profile_workspace_size(1024, C.byref(bad), C.byref(n)) == N.DCP_ERR_UNSUPPORTED
+    bad = N.ProfileOpts(2, 128, 0, 0.0, 1, 0, 0, 0, 0, 0)
+    assert lib.dcp_profile_workspace_size(1024, C.byref(bad), C.byref(n)) == N.DCP_ERR_INVALID
+    lens = np.array([64, 0], dtype=np.int64)
+    rows = (N.CostRow * 2)()
+    assert lib.dcp_profile_cost(lens.ctypes.data_as(C.POINTER(C.c_int64)), 2, C.byref(o), 1 << 20, n.value, None,
+                                rows) == N.DCP_ERR_INVALID

@@ -1,0 +1,98 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle,
+element by element, on seeded bf16 inputs.
+
+Sizes span several tiles with ragged tails; edge cases cover empty
+sequences, length-1 sequences, tile boundaries, many tiny sequences and
+causal masking.  Guard rows past the packed batch must stay untouched.
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+from oracle import attention as A
+from paper_2608_07524_amd import inputs as I
+
+from gpu_util import GRAD_TOL, LSE_TOL, O_TOL, grad_err, max_abs, to_bits, to_device
+
+pytestmark = pytest.mark.gpu
+
+GUARD = 37  # rows past the packed batch, filled with a sentinel
+
+
+@pytest.fixture(scope="module")
+def torch():
+    t = pytest.importorskip("torch")
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_07524_amd as P
+    P.load()
+    return t
+
+
+def _run_case(torch, lengths, H, D, causal, scale=None, seed=0):
+    import paper_2608_07524_amd as P
+    rng = np.random.default_rng(seed)
+    cu = I.cu_from_lengths(lengths)
+    n = int(cu[-1])
+    T = n + GUARD
+    bits = I.tensors(rng, T, H, D)
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    q, k, v, do = (to_device(torch, b) for b in bits)
+    sentinel = torch.full((T, H, D), 7.0, dtype=torch.bfloat16, device="cuda")
+    o, dq, dk, dv = (sentinel.clone() for _ in range(4))
+    lse = torch.full((H, T), 7.0, dtype=torch.float32, device="cuda")
+    P.varlen_attn_fwd(q, k, v, cu, scale, causal, out=o, lse=lse)
+    P.varlen_attn_bwd(do, o, lse, q, k, v, cu, scale, causal, dq=dq, dk=dk, dv=dv)
+    torch.cuda.synchronize()
+    got = dict(o=to_bits(o), lse=lse.cpu().numpy(), dq=to_bits(dq), dk=to_bits(dk), dv=to_bits(dv))
+    # guard rows untouched
+    for name in ("o", "dq", "dk", "dv"):
+        assert np.all(I.bf16_to_f64(got[name][n:]) == 7.0), f"{name} wrote past the packed batch"
+    assert np.all(got["lse"][:, n:] == 7.0)
+    f = [I.bf16_to_f64(b[:n]) for b in bits]
+    ref_o, ref_lse = A.attention_forward(f[0], f[1], f[2], cu, scale, causal)
+    ref_g = A.attention_backward(f[3], f[0], f[1], f[2], cu, scale, causal)
+    return got, (ref_o, ref_lse) + tuple(ref_g), n
+
+
+def _assert_close(got, ref, n, label):
+    ref_o, ref_lse, ref_dq, ref_dk, ref_dv = ref
+    eo = max_abs(got["o"][:n], ref_o)
+    el = float(np.max(np.abs(got["lse"][:, :n] - ref_lse))) if n else 0.0
+    eq = grad_err(got["dq"][:n], ref_dq) if n else 0.0
+    ek = grad_err(got["dk"][:n], ref_dk) if n else 0.0
+    ev = grad_err(got["dv"][:n], ref_dv) if n else 0.0
+    print(f"{label}: O {eo:.2e} LSE {el:.2e} dQ {eq:.2e} dK {ek:.2e} dV {ev:.2e}", flush=True)
+    assert eo <= O_TOL and el <= LSE_TOL
+    assert eq <= GRAD_TOL and ek <= GRAD_TOL and ev <= GRAD_TOL
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_tiny_packed_config(torch, causal):
+    """4 sequences {37, 64, 128, 200}, 4 heads of width 64, scale 1/8."""
+    w = I.tiny()
+    got, ref, n = _run_case(torch, w.lengths, w.n_heads, w.head_dim, causal, w.scale)
+    _assert_close(got, ref, n, f"tiny causal={causal}")
+
+
+@pytest.mark.parametrize("D", [64, 72, 128])
+@pytest.mark.parametrize("causal", [False, True])
+def test_ragged_tiles(torch, D, causal):
+    # lengths straddle the 256-row forward tile and the 128/64-row backward tiles
+    lengths = [1, 0, 255, 257, 129, 63, 65, 300, 0, 2]
+    got, ref, n = _run_case(torch, lengths, 3, D, causal, seed=D)
+    _assert_close(got, ref, n, f"ragged D={D} causal={causal}")
+
+
+def test_many_tiny_sequences(torch):
+    rng = np.random.default_rng(5)
+    lengths = rng.integers(1, 17, 300).tolist()
+    got, ref, n = _run_case(torch, lengths, 2, 72, False, seed=3)
+    _assert_close(got, ref, n, "300 seqs of 1..16")
+
+
+def test_single_long_sequence(torch):
+    got, ref, n = _run_case(torch, [1500], 2, 128, False, seed=9)
+    _assert_close(got, ref, n, "one 1500-token sequence")
