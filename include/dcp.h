@@ -122,6 +122,18 @@ int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, const void*
                         const void* q, const void* k, const void* v, void* dq, void* dk, void* dv,
                         void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Instrumentation hook for profilers and benchmarks.  begin/end are
+ * hipEvent_t handles (as void*) created by the caller.  While set on the
+ * calling thread, every dcp_varlen_attn_fwd call records `begin` right
+ * before its attention kernel and `end` right after it, and every
+ * dcp_varlen_attn_bwd call does the same around its main kernel (the one
+ * forming dQ, dK, dV), on the call's stream; the small pre/post passes and
+ * the work-list upload fall outside the pair.  Passing NULL, NULL clears the
+ * hook.  Costs two event records per call while set, nothing otherwise.
+ */
+int dcp_set_kernel_events(void* begin, void* end);
+
 /* ------------------------------------------------------------------------ */
 /* Per-length cost profile (Sec. 3.5)                                        */
 /* ------------------------------------------------------------------------ */

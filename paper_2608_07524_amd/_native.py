@@ -93,6 +93,7 @@ def load() -> C.CDLL:
         "dcp_varlen_attn_bwd_workspace_size": ([C.POINTER(AttnDesc), C.POINTER(sz)], C.c_int),
         "dcp_varlen_attn_fwd": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp, sz, vp], C.c_int),
         "dcp_varlen_attn_bwd": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], C.c_int),
+        "dcp_set_kernel_events": ([vp, vp], C.c_int),
         "dcp_profile_workspace_size": ([C.c_int64, C.POINTER(ProfileOpts), C.POINTER(sz)], C.c_int),
         "dcp_profile_cost": ([C.POINTER(C.c_int64), C.c_int32, C.POINTER(ProfileOpts), vp, sz, vp,
                               C.POINTER(CostRow)], C.c_int),
@@ -244,6 +245,14 @@ class PreparedAttention:
     def step(self):
         self.fwd()
         self.bwd()
+
+
+def set_kernel_events(begin=None, end=None):
+    """Record the hipEvent_t handles ``begin``/``end`` (ints) around each
+    following call's main attention kernel; ``None`` clears the hook (see
+    dcp_set_kernel_events)."""
+    _check(load().dcp_set_kernel_events(None if begin is None else C.c_void_p(begin),
+                                        None if end is None else C.c_void_p(end)))
 
 
 # ---------------------------------------------------------------------------

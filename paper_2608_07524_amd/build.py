@@ -48,23 +48,25 @@ def _compile(hipcc: str, src: str, obj: str, extra):
     return err
 
 
-def build(verbose: bool = False, extra=()) -> str:
+def build(verbose: bool = False, extra=(), out: str = LIB, build_dir: str = BUILD_DIR) -> str:
+    """Compile and link; ``extra`` flags go to every compile (e.g. tile-shape
+    -D overrides), ``out`` is the library path."""
     hipcc = _hipcc()
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    objs = [os.path.join(BUILD_DIR, os.path.splitext(s)[0] + ".o") for s in SOURCES]
+    os.makedirs(build_dir, exist_ok=True)
+    objs = [os.path.join(build_dir, os.path.splitext(s)[0] + ".o") for s in SOURCES]
     with ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
         logs = list(ex.map(lambda so: _compile(hipcc, so[0], so[1], list(extra)), zip(SOURCES, objs)))
     if verbose:
         for s, log in zip(SOURCES, logs):
             if log.strip():
                 print(f"--- {s}\n{log}", file=sys.stderr)
-    tmp = LIB + ".tmp"
+    tmp = out + ".tmp"
     cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stderr}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

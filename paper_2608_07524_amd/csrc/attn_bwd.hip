@@ -1,37 +1,58 @@
-// Varlen attention backward on CDNA4 for the loss <dO, O>.
+// Varlen attention backward on CDNA4 for the loss <dO, O> (gradients of the
+// exact attention the paper trains with, Sec. 4.1; block diagonal over the
+// packed sequences of Sec. 1).
 //
-// Three launches:
-//   1. bwd_pre:    Delta = rowsum(dO o O) per (row, head) in fp32 and the
-//                  fp32 dQ accumulator zeroed (rows of sequences only).
-//   2. bwd_main:   one workgroup per (key tile of kBwdBN rows, head); each of
-//                  the four wavefronts keeps 32 keys' K and V fragments and
-//                  their dK, dV accumulators in registers and walks the
-//                  query tiles of the same sequence (only those on or below
-//                  the diagonal when causal):
-//                    S  = Q K^T,  dP = dO V^T        (A from LDS, B in regs)
-//                    P  = exp2(S*scale*log2e - LSE*log2e)   (recomputed)
+// Three launches, no atomics, bitwise deterministic:
+//   1. bwd_delta:  Delta = rowsum(dO o O) per (row, head), fp32.
+//   2. bwd_dkdv:   key-stationary.  One workgroup per (key tile of 32*NW
+//                  rows, head); each wavefront keeps 32 keys' K and V
+//                  fragments and their dK, dV accumulators in registers and
+//                  walks the query tiles of its own sequence (on or below the
+//                  diagonal when causal), Q / dO tiles double-buffered in LDS:
+//                    S  = Q K^T,  dP = dO V^T         (A from LDS, B in regs)
+//                    P  = exp2(S*scale*log2e - LSE*log2e)
 //                    dS = P o (dP - Delta)
-//                    dV += P^T dO,  dK += dS^T Q      (B via transposing
-//                                                      LDS reads)
-//                  dS is staged in LDS; the workgroup then forms
-//                  dQ_tile = dS K over all its keys and adds it to the fp32
-//                  accumulator with one atomic per element.
-//   3. bwd_post:   dQ = bf16(scale * accumulator).
-// In the S / dP accumulators a lane holds one key and 16 queries, which is
-// exactly the A-operand layout P^T and dS^T need for dV and dK.
+//                    dV += P^T dO,  dK += dS^T Q       (B via transposing reads)
+//                  In the S / dP accumulators a lane holds one key and 16
+//                  queries: exactly the A-operand layout P^T and dS^T need.
+//   3. bwd_dq:     query-stationary, shaped like the forward.  One workgroup
+//                  per (query tile of 32*NW rows, head); each wavefront keeps
+//                  32 queries' Q and dO fragments, LSE, Delta and its dQ^T
+//                  accumulator in registers while K / V tiles stream through
+//                  LDS:
+//                    S^T = K Q^T,  dP^T = V dO^T       (A from LDS, B in regs)
+//                    dS^T = exp2(S^T*c - LSE*log2e) o (dP^T - Delta)
+//                    dQ^T += K^T dS^T                  (A via transposing reads,
+//                                                       B = dS^T from registers)
+// The dQ pass recomputes S and dP (two extra products) instead of adding
+// per-key-tile partial dQ into an fp32 accumulator with atomics.
 #include "attn_common.h"
 #include "attn_launch.h"
 
 namespace dcp {
 namespace {
 
-// ---------------------------------------------------------------------------
-// 1. Delta = rowsum(dO o O); zero the dQ accumulator.
-// 16 lanes per (row, head); lane c covers elements 8c .. 8c+7.
 template <int D>
-__global__ __launch_bounds__(256) void bwd_pre_kernel(const __bf16* __restrict__ dout, const __bf16* __restrict__ o,
-                                                      float* __restrict__ delta, float* __restrict__ dq_acc,
-                                                      int rows_end, int H, int T) {
+struct BwdShape {
+  static constexpr int DP = (D + 15) / 16 * 16;  // contraction width (zero padded)
+  static constexpr int NKD = DP / 16;
+  static constexpr int NDB = (D + 31) / 32;  // 32-column blocks of dK, dV, dQ
+  static constexpr int CPR = D / 8;          // 16-byte chunks per row
+  // Row strides (elements).  Rows read 16 B per lane want an odd multiple
+  // of 16 bytes; rows read by transposing 8-byte reads (4 rows x 64 B per
+  // half-wavefront) want 64 mod 128 bytes.  Tiles read both ways take the
+  // first and cover NDB*32 columns.
+  static constexpr int W = (DP > NDB * 32) ? DP : NDB * 32;
+  static constexpr int RSTR = W + 8;                                  // both ways
+  static constexpr int TSTR = (NDB * 32 % 64 == 32) ? NDB * 32 : NDB * 32 + 32;  // transposing only
+};
+
+// ---------------------------------------------------------------------------
+// 1. Delta = rowsum(dO o O); 16 lanes per (row, head), lane c covers 8c..8c+7.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict__ dout,
+                                                        const __bf16* __restrict__ o, float* __restrict__ delta,
+                                                        int rows_end, int H, int T) {
   constexpr int CPR = D / 8;
   const int64_t pair = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) >> 4;
   const int c = threadIdx.x & 15;
@@ -43,8 +64,6 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const __bf16* __restrict__
     const bf16x8 b = *reinterpret_cast<const bf16x8*>(o + off);
 #pragma unroll
     for (int e = 0; e < 8; ++e) part = fmaf(float(a[e]), float(b[e]), part);
-    *reinterpret_cast<f32x4*>(dq_acc + off) = f32x4{};
-    *reinterpret_cast<f32x4*>(dq_acc + off + 4) = f32x4{};
   }
   part += __shfl_xor(part, 8, 16);
   part += __shfl_xor(part, 4, 16);
@@ -57,56 +76,63 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const __bf16* __restrict__
   }
 }
 
-// ---------------------------------------------------------------------------
-// 3. dQ = bf16(scale * accumulator), 8 elements per thread.
-__global__ __launch_bounds__(256) void bwd_post_kernel(const float* __restrict__ dq_acc, __bf16* __restrict__ dq,
-                                                       int64_t n8, float scale) {
-  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= n8) return;
-  const f32x4 a = *reinterpret_cast<const f32x4*>(dq_acc + 8 * i);
-  const f32x4 b = *reinterpret_cast<const f32x4*>(dq_acc + 8 * i + 4);
-  bf16x8 w;
+// Writes a wavefront's 32 x D fp32 accumulator block (C layout: lane (g, j)
+// holds column 32*db + j of rows 8*(r/4) + 4*g + r%4) as bf16 rows through
+// an LDS staging area of 32 rows x stride `st`, with 16-byte global stores.
+// Orders this wavefront's LDS accesses: everything issued before has
+// completed before anything after is issued.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+}
+
+template <int D, int NDB>
+__device__ __forceinline__ void store_rows_bf16(const f32x16 (&acc)[NDB], float mul, __bf16* stage, int st,
+                                                __bf16* __restrict__ base, int64_t row_stride, int n_rows,
+                                                int lane) {
+  const int g = lane >> 5, j = lane & 31;
+  wave_lds_sync();
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    w[e] = __bf16(a[e] * scale);
-    w[4 + e] = __bf16(b[e] * scale);
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = 8 * (r >> 2) + 4 * g + (r & 3);
+      stage[row * st + 32 * db + j] = __bf16(acc[db][r] * mul);
+    }
+  wave_lds_sync();
+  constexpr int CPR = D / 8;
+  for (int ch = lane; ch < 32 * CPR; ch += 64) {
+    const int row = ch / CPR, cc = ch % CPR;
+    if (row < n_rows)
+      *reinterpret_cast<u32x4*>(base + int64_t(row) * row_stride + cc * 8) =
+          *reinterpret_cast<const u32x4*>(&stage[row * st + cc * 8]);
   }
-  *reinterpret_cast<bf16x8*>(dq + 8 * i) = w;
+  wave_lds_sync();
 }
 
 // ---------------------------------------------------------------------------
-// 2. Main backward kernel.
-template <int D, bool CAUSAL>
-__global__ __launch_bounds__(256) void attn_bwd_kernel(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
-                                                       const __bf16* __restrict__ v,
-                                                       const __bf16* __restrict__ dout,
-                                                       const float* __restrict__ lse,
-                                                       const float* __restrict__ delta,
-                                                       float* __restrict__ dq_acc, __bf16* __restrict__ dk,
-                                                       __bf16* __restrict__ dv,
-                                                       const WorkUnit* __restrict__ units, int H, int T,
-                                                       float scale, float scale_log2) {
-  constexpr int DP = (D + 15) / 16 * 16;
-  constexpr int NKD = DP / 16;
-  constexpr int NDB = (D + 31) / 32;
-  constexpr int BN = kBwdBN;  // keys per workgroup (32 per wavefront)
+// 2. dK, dV (key-stationary).
+template <int D, int NW, bool CAUSAL>
+__global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_kernel(
+    const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
+    const __bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
+    __bf16* __restrict__ dk, __bf16* __restrict__ dv, const WorkUnit* __restrict__ units, int H, int T, float scale,
+    float scale_log2) {
+  using S = BwdShape<D>;
+  constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR, QSTR = S::RSTR;
+  constexpr int NT = 64 * NW;
   constexpr int BM = kBwdBM;  // queries per step
-  constexpr int KSTR = NDB * 32 + 16;
-  constexpr int QW = (DP + 8 > NDB * 32 + 8) ? DP + 8 : NDB * 32 + 8;
-  constexpr int QSTR = (QW % 16 == 8) ? QW : QW + 8;  // keeps the row stride an odd multiple of 16 bytes
-  constexpr int DSTR = BM + 8;
-  constexpr int CPR = D / 8;
-  constexpr int NCHQ = BM * CPR;  // 16-byte chunks per Q (or dO) tile
-  constexpr int CPTQ = (NCHQ + 255) / 256;
-  constexpr int NCHK = BN * CPR;
-  constexpr int CPTK = (NCHK + 255) / 256;
+  constexpr int NCHQ = BM * CPR;
+  constexpr int CPTQ = (NCHQ + NT - 1) / NT;
+  constexpr int QBUF = BM * QSTR;
 
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[BN * KSTR];
-  __shared__ __attribute__((aligned(16))) __bf16 Qs[BM * QSTR];
-  __shared__ __attribute__((aligned(16))) __bf16 dOs[BM * QSTR];
-  __shared__ __attribute__((aligned(16))) __bf16 dSs[BN * DSTR];
-  __shared__ __attribute__((aligned(16))) float lse_s[BM];
-  __shared__ __attribute__((aligned(16))) float dlt_s[BM];
+  // Q and dO tiles (double-buffered) in one array, so the epilogue can
+  // reuse the whole block as staging space.
+  __shared__ __attribute__((aligned(16))) __bf16 qdo_lds[4 * QBUF];
+  __bf16* const Qs = qdo_lds;
+  __bf16* const dOs = qdo_lds + 2 * QBUF;
+  __shared__ __attribute__((aligned(16))) float lse_s[2 * BM];
+  __shared__ __attribute__((aligned(16))) float dlt_s[2 * BM];
 
   const WorkUnit u = units[blockIdx.x];
   const int h = blockIdx.y;
@@ -125,49 +151,41 @@ __global__ __launch_bounds__(256) void attn_bwd_kernel(const __bf16* __restrict_
   const __bf16* doh = dout + int64_t(u.seq0) * ts + int64_t(h) * D;
   const float* lseh = lse + int64_t(h) * T + u.seq0;
   const float* dlth = delta + int64_t(h) * T + u.seq0;
-  float* dqh = dq_acc + int64_t(u.seq0) * ts + int64_t(h) * D;
 
-  // Zero pad columns (tile loads never write them).
-  for (int i = tid; i < BN * (KSTR - D); i += 256) Ks[(i / (KSTR - D)) * KSTR + D + i % (KSTR - D)] = __bf16(0.f);
-  for (int i = tid; i < BM * (QSTR - D); i += 256) {
-    Qs[(i / (QSTR - D)) * QSTR + D + i % (QSTR - D)] = __bf16(0.f);
-    dOs[(i / (QSTR - D)) * QSTR + D + i % (QSTR - D)] = __bf16(0.f);
+  for (int i = tid; i < 2 * BM * (QSTR - D); i += NT) {
+    const int r = i / (QSTR - D), c = D + i % (QSTR - D);
+    Qs[r * QSTR + c] = __bf16(0.f);
+    dOs[r * QSTR + c] = __bf16(0.f);
   }
-  // K tile -> LDS (rows past the sequence end are zero).
-#pragma unroll
-  for (int c = 0; c < CPTK; ++c) {
-    const int ch = tid + 256 * c;
-    if (NCHK % 256 == 0 || ch < NCHK) {
-      const int r = ch / CPR, cc = ch % CPR;
-      u32x4 val = u32x4{0, 0, 0, 0};
-      if (r < u.rows) val = *reinterpret_cast<const u32x4*>(kh + int64_t(key_t0 + r) * ts + cc * 8);
-      *reinterpret_cast<u32x4*>(&Ks[r * KSTR + cc * 8]) = val;
-    }
-  }
-  // V fragments (B operand of dP = dO V^T): lane (g, j) holds key j of this
-  // wavefront, columns 16*kd + 8*g .. +7.
+
+  // K and V fragments (B operands of S = Q K^T and dP = dO V^T): lane (g, j)
+  // holds key j of this wavefront, columns 16*kd + 8*g .. +7.
   const int my_key = 32 * wave + j;  // tile-relative
-  bf16x8 vf[NKD];
+  const bool key_ok = my_key < u.rows;
+  bf16x8 kf[NKD], vf[NKD];
 #pragma unroll
   for (int kd = 0; kd < NKD; ++kd) {
     const int col = 16 * kd + 8 * g;
-    if (my_key < u.rows && col < D) {
+    if (key_ok && col < D) {
+      kf[kd] = *reinterpret_cast<const bf16x8*>(kh + int64_t(key_t0 + my_key) * ts + col);
       vf[kd] = *reinterpret_cast<const bf16x8*>(vh + int64_t(key_t0 + my_key) * ts + col);
     } else {
+      kf[kd] = bf16x8{};
       vf[kd] = bf16x8{};
     }
   }
 
   const int q_begin = CAUSAL ? (key_t0 / BM) * BM : 0;
   const int n_qt = (seqlen - q_begin + BM - 1) / BM;
+  const int key_seq = key_t0 + my_key;
 
   u32x4 qreg[CPTQ], doreg[CPTQ];
   float lse_reg = INFINITY, dlt_reg = 0.f;
   auto load_q_tile = [&](int q0) {
 #pragma unroll
     for (int c = 0; c < CPTQ; ++c) {
-      const int ch = tid + 256 * c;
-      if (NCHQ % 256 == 0 || ch < NCHQ) {
+      const int ch = tid + NT * c;
+      if (NCHQ % NT == 0 || ch < NCHQ) {
         const int r = ch / CPR, cc = ch % CPR;
         if (q0 + r < seqlen) {
           qreg[c] = *reinterpret_cast<const u32x4*>(qh + int64_t(q0 + r) * ts + cc * 8);
@@ -185,19 +203,19 @@ __global__ __launch_bounds__(256) void attn_bwd_kernel(const __bf16* __restrict_
       dlt_reg = ok ? dlth[q0 + tid] : 0.f;
     }
   };
-  auto store_q_tile = [&]() {
+  auto store_q_tile = [&](int buf) {
 #pragma unroll
     for (int c = 0; c < CPTQ; ++c) {
-      const int ch = tid + 256 * c;
-      if (NCHQ % 256 == 0 || ch < NCHQ) {
+      const int ch = tid + NT * c;
+      if (NCHQ % NT == 0 || ch < NCHQ) {
         const int r = ch / CPR, cc = ch % CPR;
-        *reinterpret_cast<u32x4*>(&Qs[r * QSTR + cc * 8]) = qreg[c];
-        *reinterpret_cast<u32x4*>(&dOs[r * QSTR + cc * 8]) = doreg[c];
+        *reinterpret_cast<u32x4*>(&Qs[buf * QBUF + r * QSTR + cc * 8]) = qreg[c];
+        *reinterpret_cast<u32x4*>(&dOs[buf * QBUF + r * QSTR + cc * 8]) = doreg[c];
       }
     }
     if (tid < BM) {
-      lse_s[tid] = lse_reg;
-      dlt_s[tid] = dlt_reg;
+      lse_s[buf * BM + tid] = lse_reg;
+      dlt_s[buf * BM + tid] = dlt_reg;
     }
   };
 
@@ -208,126 +226,265 @@ __global__ __launch_bounds__(256) void attn_bwd_kernel(const __bf16* __restrict_
     dv_acc[db] = f32x16{};
   }
 
-  if (n_qt > 0) load_q_tile(q_begin);
-  __syncthreads();  // K tile and pads visible
-  // K fragments (B operand of S = Q K^T), same layout as vf.
-  bf16x8 kf[NKD];
-#pragma unroll
-  for (int kd = 0; kd < NKD; ++kd) kf[kd] = lds_read_b128(&Ks[my_key * KSTR + 16 * kd + 8 * g]);
+  if (n_qt > 0) {
+    load_q_tile(q_begin);
+    store_q_tile(0);
+  }
+  __syncthreads();
 
   const int tr_row = (lane & 15) >> 2;
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  const int key_seq = key_t0 + my_key;  // this lane's key, sequence-relative
-  const bool key_ok = my_key < u.rows;
+  const int wave_key_lo = key_t0 + 32 * wave;  // smallest key of this wavefront
 
   for (int it = 0; it < n_qt; ++it) {
+    const int buf = it & 1;
     const int q0 = q_begin + it * BM;
-    store_q_tile();
-    __syncthreads();
     if (it + 1 < n_qt) load_q_tile(q0 + BM);
+    const __bf16* Qb = &Qs[buf * QBUF];
+    const __bf16* dOb = &dOs[buf * QBUF];
+    const float* lseb = &lse_s[buf * BM];
+    const float* dltb = &dlt_s[buf * BM];
 
 #pragma unroll
     for (int qb = 0; qb < BM / 32; ++qb) {
+      // causal: a 32-query block entirely above this wavefront's keys adds nothing
+      if (CAUSAL && q0 + 32 * qb + 31 < wave_key_lo) continue;
       f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
       for (int kd = 0; kd < NKD; ++kd) {
-        const bf16x8 aq = lds_read_b128(&Qs[(32 * qb + j) * QSTR + 16 * kd + 8 * g]);
+        const bf16x8 aq = lds_read_b128(&Qb[(32 * qb + j) * QSTR + 16 * kd + 8 * g]);
         s = mfma32(aq, kf[kd], s);
-        const bf16x8 ado = lds_read_b128(&dOs[(32 * qb + j) * QSTR + 16 * kd + 8 * g]);
+        const bf16x8 ado = lds_read_b128(&dOb[(32 * qb + j) * QSTR + 16 * kd + 8 * g]);
         dp = mfma32(ado, vf[kd], dp);
       }
-      // Row statistics for the 16 queries this lane holds: 32qb + 8b + 4g + c.
-      float pv[16], dsv[16];
+      // This lane holds key `key_seq` against queries 32qb + 8b + 4g + c.
+      bf16x8 pa[2], da[2];
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse_s[32 * qb + 8 * b + 4 * g]);
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dlt_s[32 * qb + 8 * b + 4 * g]);
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lseb[32 * qb + 8 * b + 4 * g]);
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dltb[32 * qb + 8 * b + 4 * g]);
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           const int r = 4 * b + c;
-          float p = exp2f(fmaf(s[r], scale_log2, -l4[c]));
-          if (CAUSAL) {
-            const int qi = q0 + 32 * qb + 8 * b + 4 * g + c;
-            if (key_seq > qi) p = 0.f;
-          }
+          float p = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -l4[c]));
+          if (CAUSAL && key_seq > q0 + 32 * qb + 8 * b + 4 * g + c) p = 0.f;
           if (!key_ok) p = 0.f;
-          pv[r] = p;
-          dsv[r] = p * (dp[r] - d4[c]);
+          pa[b >> 1][4 * (b & 1) + c] = __bf16(p);
+          da[b >> 1][4 * (b & 1) + c] = __bf16(p * (dp[r] - d4[c]));
         }
       }
-      bf16x8 pa[2], da[2];
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          pa[hh][e] = __bf16(pv[8 * hh + e]);
-          da[hh][e] = __bf16(dsv[8 * hh + e]);
-        }
-      // dV += P^T dO and dK += dS^T Q; B = rows (queries) x columns (d)
+      // dV += P^T dO and dK += dS^T Q: B = rows (queries) x columns (d),
       // fetched column-wise with transposing reads.
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
           const int off = (32 * qb + 16 * hh + 4 * g + tr_row) * QSTR + 32 * db + tr_col;
-          const bf16x8 bdo = cat(lds_read_tr(&dOs[off]), lds_read_tr(&dOs[off + 8 * QSTR]));
+          const bf16x8 bdo = cat(lds_read_tr(&dOb[off]), lds_read_tr(&dOb[off + 8 * QSTR]));
           dv_acc[db] = mfma32(pa[hh], bdo, dv_acc[db]);
-          const bf16x8 bq = cat(lds_read_tr(&Qs[off]), lds_read_tr(&Qs[off + 8 * QSTR]));
+          const bf16x8 bq = cat(lds_read_tr(&Qb[off]), lds_read_tr(&Qb[off + 8 * QSTR]));
           dk_acc[db] = mfma32(da[hh], bq, dk_acc[db]);
         }
       }
-      // Stage dS as [key][query] for the dQ product.
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        bf16x4 w;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) w[c] = da[b >> 1][4 * (b & 1) + c];
-        *reinterpret_cast<bf16x4*>(&dSs[my_key * DSTR + 32 * qb + 8 * b + 4 * g]) = w;
-      }
     }
-    __syncthreads();
-
-    // dQ_tile = dS K over the workgroup's BN keys; (query block, d block)
-    // jobs are spread over the wavefronts.
-    for (int job = wave; job < (BM / 32) * NDB; job += 4) {
-      const int qb = job / NDB, db = job % NDB;
-      f32x16 acc = f32x16{};
-#pragma unroll
-      for (int kk = 0; kk < BN / 16; ++kk) {
-        const int arow = 16 * kk + 4 * g + tr_row;
-        const __bf16* pa_ = &dSs[arow * DSTR + 32 * qb + tr_col];
-        const bf16x8 a = cat(lds_read_tr(pa_), lds_read_tr(pa_ + 8 * DSTR));
-        const __bf16* pb_ = &Ks[arow * KSTR + 32 * db + tr_col];
-        const bf16x8 b = cat(lds_read_tr(pb_), lds_read_tr(pb_ + 8 * KSTR));
-        acc = mfma32(a, b, acc);
-      }
-      const int d = 32 * db + j;
-      if (d < D) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int qi = q0 + 32 * qb + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (qi < seqlen) atomic_add_f32(dqh + int64_t(qi) * ts + d, acc[r]);
-        }
-      }
-    }
+    if (it + 1 < n_qt) store_q_tile(buf ^ 1);
     __syncthreads();
   }
 
-  // Epilogue: lane (g, j) holds column 32*db + j of keys 8*(r/4) + 4*g + r%4.
+  // Epilogue through LDS (the Q / dO buffers are free now): each wavefront
+  // stages its 32 rows of dK, then of dV.
+  static_assert(4 * QBUF >= NW * 32 * QSTR, "staging area too small");
+  __bf16* stage = qdo_lds + wave * 32 * QSTR;  // 32 rows per wavefront
+  const int n_rows = max(0, min(32, u.rows - 32 * wave));
+  __bf16* dk_base = dk + int64_t(u.row0 + 32 * wave) * ts + int64_t(h) * D;
+  __bf16* dv_base = dv + int64_t(u.row0 + 32 * wave) * ts + int64_t(h) * D;
+  store_rows_bf16<D, NDB>(dk_acc, scale, stage, QSTR, dk_base, ts, n_rows, lane);
+  store_rows_bf16<D, NDB>(dv_acc, 1.f, stage, QSTR, dv_base, ts, n_rows, lane);
+}
+
+// ---------------------------------------------------------------------------
+// 3. dQ (query-stationary).
+template <int D, int NW, bool CAUSAL>
+__global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
+    const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
+    const __bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
+    __bf16* __restrict__ dq, const WorkUnit* __restrict__ units, int H, int T, float scale, float scale_log2) {
+  using S = BwdShape<D>;
+  constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
+  constexpr int KSTR = S::DP + 8;  // K and V rows read 16 B per lane
+  constexpr int TSTR = S::TSTR;    // second copy of K for transposing reads
+  constexpr int BN = kBwdDqBN;
+  constexpr int NT = 64 * NW;
+  constexpr int NCH = BN * CPR;
+  constexpr int CPT = (NCH + NT - 1) / NT;
+  constexpr int KBUF = BN * KSTR, TBUF = BN * TSTR;
+
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[2 * KBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[2 * KBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 Kt[2 * TBUF];
+
+  const WorkUnit u = units[blockIdx.x];
+  const int h = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int g = lane >> 5;
+  const int j = lane & 31;
+  const int64_t ts = int64_t(H) * D;
+  const int seqlen = u.seqlen;
+  const int tile_q0 = u.row0 - u.seq0;
+  const int wave_q0 = tile_q0 + 32 * wave;
+
+  const __bf16* qh = q + int64_t(u.seq0) * ts + int64_t(h) * D;
+  const __bf16* kh = k + int64_t(u.seq0) * ts + int64_t(h) * D;
+  const __bf16* vh = v + int64_t(u.seq0) * ts + int64_t(h) * D;
+  const __bf16* doh = dout + int64_t(u.seq0) * ts + int64_t(h) * D;
+
+  for (int i = tid; i < 2 * BN * (KSTR - D); i += NT) {
+    const int r = i / (KSTR - D), c = D + i % (KSTR - D);
+    Ks[r * KSTR + c] = __bf16(0.f);
+    Vs[r * KSTR + c] = __bf16(0.f);
+  }
+  for (int i = tid; i < 2 * BN * (TSTR - D); i += NT) {
+    const int r = i / (TSTR - D), c = D + i % (TSTR - D);
+    Kt[r * TSTR + c] = __bf16(0.f);
+  }
+
+  // Per-lane query state: Q and dO fragments (B operands), LSE, Delta.
+  const int qrel = 32 * wave + j;
+  const bool q_ok = qrel < u.rows;
+  const int my_q = tile_q0 + qrel;  // sequence-relative
+  bf16x8 qf[NKD], df[NKD];
 #pragma unroll
-  for (int db = 0; db < NDB; ++db) {
-    const int d = 32 * db + j;
-    if (d < D) {
+  for (int kd = 0; kd < NKD; ++kd) {
+    const int col = 16 * kd + 8 * g;
+    if (q_ok && col < D) {
+      qf[kd] = *reinterpret_cast<const bf16x8*>(qh + int64_t(my_q) * ts + col);
+      df[kd] = *reinterpret_cast<const bf16x8*>(doh + int64_t(my_q) * ts + col);
+    } else {
+      qf[kd] = bf16x8{};
+      df[kd] = bf16x8{};
+    }
+  }
+  const float lse2 = q_ok ? lse[int64_t(h) * T + u.seq0 + my_q] * kLog2e : INFINITY;
+  const float dlt = q_ok ? delta[int64_t(h) * T + u.seq0 + my_q] : 0.f;
+
+  const int key_end = CAUSAL ? min(seqlen, tile_q0 + u.rows) : seqlen;
+  const int n_tiles = (key_end + BN - 1) / BN;
+
+  u32x4 kreg[CPT], vreg[CPT];
+  auto load_tile = [&](int kt) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = 32 * wave + 8 * (r >> 2) + 4 * g + (r & 3);
-        if (key < u.rows) {
-          const int64_t off = int64_t(u.row0 + key) * ts + int64_t(h) * D + d;
-          dk[off] = __bf16(dk_acc[db][r] * scale);
-          dv[off] = __bf16(dv_acc[db][r]);
+    for (int c = 0; c < CPT; ++c) {
+      const int ch = tid + NT * c;
+      if (NCH % NT == 0 || ch < NCH) {
+        const int r = ch / CPR, cc = ch % CPR;
+        const int key = kt * BN + r;
+        if (key < seqlen) {
+          kreg[c] = *reinterpret_cast<const u32x4*>(kh + int64_t(key) * ts + cc * 8);
+          vreg[c] = *reinterpret_cast<const u32x4*>(vh + int64_t(key) * ts + cc * 8);
+        } else {
+          kreg[c] = u32x4{0, 0, 0, 0};
+          vreg[c] = u32x4{0, 0, 0, 0};
         }
       }
     }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) {
+      const int ch = tid + NT * c;
+      if (NCH % NT == 0 || ch < NCH) {
+        const int r = ch / CPR, cc = ch % CPR;
+        *reinterpret_cast<u32x4*>(&Ks[buf * KBUF + r * KSTR + cc * 8]) = kreg[c];
+        *reinterpret_cast<u32x4*>(&Vs[buf * KBUF + r * KSTR + cc * 8]) = vreg[c];
+        *reinterpret_cast<u32x4*>(&Kt[buf * TBUF + r * TSTR + cc * 8]) = kreg[c];
+      }
+    }
+  };
+
+  f32x16 acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
+
+  if (n_tiles > 0) {
+    load_tile(0);
+    store_tile(0);
+  }
+  __syncthreads();
+
+  const int tr_row = (lane & 15) >> 2;
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const int wave_last_q = wave_q0 + 31;
+
+  for (int kt = 0; kt < n_tiles; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < n_tiles) load_tile(kt + 1);
+    const int k0 = kt * BN;
+    if (!CAUSAL || k0 <= wave_last_q) {
+      const __bf16* Kb = &Ks[buf * KBUF];
+      const __bf16* Vb = &Vs[buf * KBUF];
+      const __bf16* Tb = &Kt[buf * TBUF];
+      f32x16 s[BN / 32], dp[BN / 32];
+#pragma unroll
+      for (int kb = 0; kb < BN / 32; ++kb) {
+        s[kb] = f32x16{};
+        dp[kb] = f32x16{};
+      }
+#pragma unroll
+      for (int kd = 0; kd < NKD; ++kd) {
+#pragma unroll
+        for (int kb = 0; kb < BN / 32; ++kb) {
+          const bf16x8 ak = lds_read_b128(&Kb[(32 * kb + j) * KSTR + 16 * kd + 8 * g]);
+          s[kb] = mfma32(ak, qf[kd], s[kb]);
+          const bf16x8 av = lds_read_b128(&Vb[(32 * kb + j) * KSTR + 16 * kd + 8 * g]);
+          dp[kb] = mfma32(av, df[kd], dp[kb]);
+        }
+      }
+      const bool need_mask = (k0 + BN > seqlen) || (CAUSAL && k0 + BN - 1 > wave_q0);
+      bf16x8 dsb[BN / 32][2];
+#pragma unroll
+      for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], scale_log2, -lse2));
+          if (need_mask) {
+            const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * g + (r & 3);
+            if (key >= seqlen || (CAUSAL && key > my_q)) p = 0.f;
+          }
+          dsb[kb][r >> 3][r & 7] = __bf16(p * (dp[kb][r] - dlt));
+        }
+      // dQ^T += K^T dS^T: A = K^T (rows d, keys 32kb + 16hh + 4g + {0..3, 8..11}).
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const __bf16* p = &Tb[(32 * kb + 16 * hh + 4 * g + tr_row) * TSTR + 32 * db + tr_col];
+            const bf16x8 a = cat(lds_read_tr(p), lds_read_tr(p + 8 * TSTR));
+            acc[db] = mfma32(a, dsb[kb][hh], acc[db]);
+          }
+    }
+    if (kt + 1 < n_tiles) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  // Epilogue: lane (g, j) holds query j, columns 32db + 8rb + 4g + {0..3}.
+  if (q_ok) {
+    __bf16* qrow = dq + int64_t(u.seq0 + my_q) * ts + int64_t(h) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        const int d0 = 32 * db + 8 * rb + 4 * g;
+        if (d0 < D) {
+          bf16x4 w;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) w[c] = __bf16(acc[db][4 * rb + c] * scale);
+          *reinterpret_cast<bf16x4*>(qrow + d0) = w;
+        }
+      }
   }
 }
 
@@ -336,27 +493,35 @@ hipError_t launch_bwd_t(const BwdArgs& a) {
   const int64_t n_pairs = int64_t(a.rows_end) * a.n_heads;
   if (n_pairs > 0) {
     const int64_t blocks = (n_pairs * 16 + 255) / 256;
-    hipLaunchKernelGGL((bwd_pre_kernel<D>), dim3(unsigned(blocks)), dim3(256), 0, a.stream,
-                       static_cast<const __bf16*>(a.dout), static_cast<const __bf16*>(a.o), a.delta, a.dq_acc,
-                       a.rows_end, a.n_heads, a.total_tokens);
+    hipLaunchKernelGGL((bwd_delta_kernel<D>), dim3(unsigned(blocks)), dim3(256), 0, a.stream,
+                       static_cast<const __bf16*>(a.dout), static_cast<const __bf16*>(a.o), a.delta, a.rows_end,
+                       a.n_heads, a.total_tokens);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  const KernelEvents& ev = kernel_events();
   if (a.n_units > 0) {
-    hipLaunchKernelGGL((attn_bwd_kernel<D, CAUSAL>), dim3(a.n_units, a.n_heads), dim3(256), 0, a.stream,
-                       static_cast<const __bf16*>(a.q), static_cast<const __bf16*>(a.k),
-                       static_cast<const __bf16*>(a.v), static_cast<const __bf16*>(a.dout), a.lse, a.delta,
-                       a.dq_acc, static_cast<__bf16*>(a.dk), static_cast<__bf16*>(a.dv),
-                       static_cast<const WorkUnit*>(a.units), a.n_heads, a.total_tokens, a.scale,
+    if (ev.begin) (void)hipEventRecord(ev.begin, a.stream);
+    constexpr int NW = bwd_dkdv_waves(D);
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, NW, CAUSAL>), dim3(a.n_units, a.n_heads), dim3(64 * NW), 0,
+                       a.stream, static_cast<const __bf16*>(a.q),
+                       static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
+                       static_cast<const __bf16*>(a.dout), a.lse, a.delta, static_cast<__bf16*>(a.dk),
+                       static_cast<__bf16*>(a.dv), static_cast<const WorkUnit*>(a.units), a.n_heads,
+                       a.total_tokens, a.scale, a.scale * kLog2e);
+    hipError_t e = hipGetLastError();
+    if (ev.end) (void)hipEventRecord(ev.end, a.stream);
+    if (e != hipSuccess) return e;
+  }
+  if (a.n_qunits > 0) {
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, kBwdDqWaves, CAUSAL>), dim3(a.n_qunits, a.n_heads),
+                       dim3(64 * kBwdDqWaves), 0, a.stream, static_cast<const __bf16*>(a.q),
+                       static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
+                       static_cast<const __bf16*>(a.dout), a.lse, a.delta, static_cast<__bf16*>(a.dq),
+                       static_cast<const WorkUnit*>(a.qunits), a.n_heads, a.total_tokens, a.scale,
                        a.scale * kLog2e);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-  }
-  const int64_t n8 = n_pairs * D / 8;
-  if (n8 > 0) {
-    hipLaunchKernelGGL(bwd_post_kernel, dim3(unsigned((n8 + 255) / 256)), dim3(256), 0, a.stream, a.dq_acc,
-                       static_cast<__bf16*>(a.dq), n8, a.scale);
-    return hipGetLastError();
   }
   return hipSuccess;
 }
@@ -376,6 +541,9 @@ __global__ void fill_bf16_kernel(__bf16* p, int64_t n, uint32_t seed) {
 }
 
 }  // namespace
+
+int bwd_key_tile_rows(int head_dim) { return 32 * bwd_dkdv_waves(head_dim); }
+int bwd_query_tile_rows(int head_dim) { return 32 * kBwdDqWaves; }
 
 hipError_t launch_bwd(const BwdArgs& a) {
   switch (a.head_dim) {

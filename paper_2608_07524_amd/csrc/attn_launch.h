@@ -6,12 +6,28 @@
 
 namespace dcp {
 
-// Query rows per forward workgroup: 4 wavefronts x 32 x kFwdNQB.
-constexpr int kFwdNQB = 2;
-// Key rows per backward workgroup (4 wavefronts x 32) and query rows per
-// backward inner step.
-constexpr int kBwdBN = 128;
+// Query rows per forward workgroup: kFwdWaves wavefronts x 32 x kFwdNQB.
+#ifndef DCP_FWD_NQB
+#define DCP_FWD_NQB 1
+#endif
+#ifndef DCP_FWD_WAVES
+#define DCP_FWD_WAVES 8
+#endif
+constexpr int kFwdNQB = DCP_FWD_NQB;
+constexpr int kFwdWaves = DCP_FWD_WAVES;
+// Backward: kBwdWaves wavefronts per workgroup, 32 keys (dK/dV pass) or 32
+// queries (dQ pass) each; the dK/dV pass steps over kBwdBM queries at a
+// time, the dQ pass over kBwdDqBN keys.
+// The dK/dV pass keeps K, V fragments and dK, dV accumulators resident; at
+// head width 128 they do not fit the 256 registers of two wavefronts per
+// SIMD, so that width runs one wavefront per SIMD.
+#ifndef DCP_BWD_WAVES_D128
+#define DCP_BWD_WAVES_D128 4
+#endif
+constexpr int bwd_dkdv_waves(int head_dim) { return head_dim > 96 ? DCP_BWD_WAVES_D128 : 8; }
+constexpr int kBwdDqWaves = 8;
 constexpr int kBwdBM = 64;
+constexpr int kBwdDqBN = 64;
 
 struct FwdArgs {
   const void* q;
@@ -39,10 +55,11 @@ struct BwdArgs {
   void* dq;
   void* dk;
   void* dv;
-  float* dq_acc;          // fp32 [T, H, D] workspace
   float* delta;           // fp32 [H, T] workspace
-  const void* units;      // device WorkUnit[n_units], key tiles of kBwdBN rows
+  const void* units;      // device WorkUnit[n_units], key tiles
   int n_units;
+  const void* qunits;     // device WorkUnit[n_qunits], query tiles
+  int n_qunits;
   int rows_end;           // cu_seqlens[n]: rows past it are not touched
   int n_heads;
   int head_dim;
@@ -52,7 +69,17 @@ struct BwdArgs {
   hipStream_t stream;
 };
 
+// Optional events recorded around the main attention kernel of each call
+// (set through dcp_set_kernel_events; null when unused).
+struct KernelEvents {
+  hipEvent_t begin = nullptr;
+  hipEvent_t end = nullptr;
+};
+KernelEvents& kernel_events();
+
 int fwd_tile_rows(int head_dim);
+int bwd_key_tile_rows(int head_dim);
+int bwd_query_tile_rows(int head_dim);
 hipError_t launch_fwd(const FwdArgs& a);
 hipError_t launch_bwd(const BwdArgs& a);
 

@@ -32,6 +32,11 @@ int fail(int code, const char* fmt, ...) {
 
 void clear_error() { g_last_error.clear(); }
 
+KernelEvents& kernel_events() {
+  thread_local KernelEvents ev;
+  return ev;
+}
+
 namespace {
 
 constexpr size_t kAlign = 256;
@@ -125,15 +130,14 @@ size_t count_units(const dcp_attn_desc* d, int tile) {
 }
 
 struct BwdLayout {
-  size_t delta, dq_acc, units, total;
+  size_t delta, units, qunits, total;
 };
 BwdLayout bwd_layout(const dcp_attn_desc* d) {
   BwdLayout l;
-  const int64_t rows_end = d->cu_seqlens_host[d->n_seqs];
   l.delta = 0;
-  l.dq_acc = align_up(size_t(4) * size_t(d->n_heads) * size_t(d->total_tokens));
-  l.units = l.dq_acc + align_up(size_t(4) * size_t(rows_end) * size_t(d->n_heads) * size_t(d->head_dim));
-  l.total = l.units + align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, kBwdBN)));
+  l.units = align_up(size_t(4) * size_t(d->n_heads) * size_t(d->total_tokens));
+  l.qunits = l.units + align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, bwd_key_tile_rows(d->head_dim))));
+  l.total = l.qunits + align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, bwd_query_tile_rows(d->head_dim))));
   return l;
 }
 
@@ -152,6 +156,14 @@ using namespace dcp;
 extern "C" const char* dcp_last_error(void) { return g_last_error.c_str(); }
 
 extern "C" const char* dcp_version(void) { return "dcp-mi355x 0.1 (gfx950)"; }
+
+extern "C" int dcp_set_kernel_events(void* begin, void* end) {
+  clear_error();
+  if ((begin == nullptr) != (end == nullptr)) return fail(DCP_ERR_INVALID, "set both events or neither");
+  kernel_events().begin = static_cast<hipEvent_t>(begin);
+  kernel_events().end = static_cast<hipEvent_t>(end);
+  return DCP_OK;
+}
 
 extern "C" int dcp_varlen_attn_fwd_workspace_size(const dcp_attn_desc* desc, size_t* bytes) {
   clear_error();
@@ -213,13 +225,15 @@ extern "C" int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, 
     return fail(DCP_ERR_WORKSPACE, "backward workspace needs %zu bytes, got %zu", l.total, workspace_bytes);
   if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(DCP_ERR_INVALID, "workspace must be 16-byte aligned");
   if ((st = check_device())) return st;
-  const std::vector<WorkUnit> units = build_units(desc, kBwdBN, true);
+  const std::vector<WorkUnit> units = build_units(desc, bwd_key_tile_rows(desc->head_dim), true);
   if (units.empty()) return DCP_OK;
+  const std::vector<WorkUnit> qunits = build_units(desc, bwd_query_tile_rows(desc->head_dim), false);
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
   if ((st = upload_units(units, ws + l.units, s))) return st;
-  BwdArgs a{dout, o, lse, q, k, v, dq, dk, dv, reinterpret_cast<float*>(ws + l.dq_acc),
-            reinterpret_cast<float*>(ws + l.delta), ws + l.units, int(units.size()),
+  if ((st = upload_units(qunits, ws + l.qunits, s))) return st;
+  BwdArgs a{dout, o, lse, q, k, v, dq, dk, dv, reinterpret_cast<float*>(ws + l.delta),
+            ws + l.units, int(units.size()), ws + l.qunits, int(qunits.size()),
             desc->cu_seqlens_host[desc->n_seqs], desc->n_heads, desc->head_dim, int(desc->total_tokens),
             desc->scale, desc->causal, s};
   hipError_t e = launch_bwd(a);

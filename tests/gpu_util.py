@@ -8,10 +8,13 @@ import numpy as np
 from paper_2608_07524_amd import inputs as I
 
 # Tolerances: outputs max-abs 1e-2, gradients max-abs relative to the
-# largest reference magnitude 2e-2 (bf16 inputs); LSE max-abs 1e-3.
+# largest reference magnitude 2e-2 (bf16 inputs).  LSE: the row sum is taken
+# over bf16-rounded probabilities (the same weights that form O), each off by
+# at most 2^-8 relative, so |dLSE| <= -ln(1 - 2^-8) = 3.9e-3; 5e-3 leaves room
+# for fp32 accumulation and stays inside the 1e-2 output bound.
 O_TOL = 1e-2
 GRAD_TOL = 2e-2
-LSE_TOL = 1e-3
+LSE_TOL = 5e-3
 
 
 def to_device(torch, bits: np.ndarray, device="cuda"):

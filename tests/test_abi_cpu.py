@@ -74,7 +74,7 @@ def test_pointer_workspace_and_device_errors():
     assert "workspace" in P.last_error()
     nb = C.c_size_t()
     assert lib.dcp_varlen_attn_bwd_workspace_size(C.byref(d), C.byref(nb)) == 0
-    assert nb.value > 4 * 101 * 2 * 64
+    assert nb.value >= 4 * 101 * 2  # rowsum(dO o O) per (row, head)
     assert lib.dcp_varlen_attn_bwd(C.byref(d), *([fake] * 9), fake, nb.value - 1, None) == N.DCP_ERR_WORKSPACE
     # valid arguments but no gfx950 device in this process
     import torch
