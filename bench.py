@@ -31,6 +31,31 @@ if ROOT not in sys.path:
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak
 HBM_PEAK_GBS = 8000.0
 
+# HBM bytes per launch of the dK/dV kernel from two rocprofv3 --pmc passes
+# (FETCH_SIZE x 2.000 and WRITE_SIZE x 1.000, the scales a plain device copy
+# of known size reads), per workload; valid only for the kernel sources
+# whose hash is recorded with them.
+MEASURED_TRAFFIC = {
+    "video_short": {"sources_sha256_16": "72c0846f8d10a21d", "bytes": (4952468.8 * 2.0 + 691200.0) * 1024},
+}
+KERNEL_SOURCES = ("attn_bwd.hip", "attn_common.h", "attn_launch.h")
+
+
+def kernel_sources_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_07524_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload_name: str):
+    m = MEASURED_TRAFFIC.get(workload_name)
+    if m is None or m["sources_sha256_16"] != kernel_sources_hash():
+        return None
+    return m["bytes"]
+
 
 def workload(name: str, seed: int = 0):
     from paper_2608_07524_amd import inputs as I
@@ -160,6 +185,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-padded", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (a known-traffic reference for "
+                         "HBM byte counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -172,6 +200,14 @@ def main():
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
     P.load()
+
+    if args.copy_probe_mib:
+        src = torch.empty(args.copy_probe_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     w, rng = workload(args.workload, args.seed)
     H, D, causal = w.n_heads, w.head_dim, w.causal
@@ -230,7 +266,8 @@ def main():
                     "bwd_rest_ms": ms - fwd_ms - bwd_ms},
         "roofline": {"kernel": "attn_bwd_dkdv_kernel", "bound": "mfma", "achieved": dkdv_tflops,
                      "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": dkdv_tflops / BF16_PEAK_TFLOPS,
-                     "traffic": None,
+                     "traffic": measured_traffic(args.workload),
+                     "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
                      "flop_per_launch": flop_dkdv, "flop_convention": "8*pairs*H*D (S, dP, dV, dK products)"},
         "padded_baseline": padded,
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(w, args.seed),

@@ -1,0 +1,175 @@
+"""GPU parity at the benchmark's full sizes, in the launch configuration
+bench.py times.
+
+Every output the oracle can evaluate one row at a time is checked on a
+seeded sample: O, LSE and dQ rows (the first and last rows of sequences
+always included).  dK and dV rows need the whole softmax column of a key,
+so they are checked on sampled keys of sampled (sequence, head) pairs that
+the oracle finishes in seconds, plus, for every (sequence, head), the exact
+identities sum_j dV_j = sum_i dO_i and sum_j dK_j = 0.
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+from oracle import attention as A
+from paper_2608_07524_amd import inputs as I
+
+from gpu_util import GRAD_TOL, LSE_TOL, O_TOL, to_bits, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    t = pytest.importorskip("torch")
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_07524_amd as P
+    P.load()
+    return t
+
+
+def _run(torch, w, rng):
+    import paper_2608_07524_amd as P
+    T, H, D = w.total_tokens, w.n_heads, w.head_dim
+    bits = I.tensors(rng, T, H, D)
+    q, k, v, do = (to_device(torch, b) for b in bits)
+    call = P.PreparedAttention(q, k, v, do, w.cu_seqlens, w.scale, w.causal)
+    call.fwd()
+    call.bwd()
+    torch.cuda.synchronize()
+    out = dict(o=to_bits(call.o), lse=call.lse.cpu().numpy(), dq=to_bits(call.dq), dk=to_bits(call.dk),
+               dv=to_bits(call.dv))
+    del call, q, k, v, do
+    torch.cuda.empty_cache()
+    return bits, out
+
+
+def _sample_rows(rng, cu, H, n_random):
+    rows, heads = [], []
+    for b in range(len(cu) - 1):
+        if cu[b + 1] > cu[b]:
+            rows += [int(cu[b]), int(cu[b + 1]) - 1]
+            heads += [int(rng.integers(H)), int(rng.integers(H))]
+    r = rng.integers(0, int(cu[-1]), n_random)
+    rows += r.tolist()
+    heads += rng.integers(0, H, n_random).tolist()
+    return np.array(rows), np.array(heads)
+
+
+def _check_rows(bits, out, w, rng, n_random, label):
+    cu = w.cu_seqlens
+    rows, heads = _sample_rows(rng, cu, w.n_heads, n_random)
+    # float32 holds bf16 exactly; the oracle widens every slice it uses to float64
+    q, k, v, do = (I.bf16_to_f32(b) for b in bits)
+    ro, rl = A.attention_rows(q, k, v, cu, w.scale, w.causal, rows, heads)
+    rdq = A.attention_dq_rows(do, q, k, v, cu, w.scale, w.causal, rows, heads)
+    go = I.bf16_to_f64(out["o"][rows, heads])
+    gl = out["lse"][heads, rows]
+    gdq = I.bf16_to_f64(out["dq"][rows, heads])
+    eo = float(np.max(np.abs(go - ro)))
+    el = float(np.max(np.abs(gl - rl)))
+    # dQ relative to the largest reference magnitude over the sampled rows
+    edq = float(np.max(np.abs(gdq - rdq)) / np.max(np.abs(rdq)))
+    print(f"{label}: {rows.size} sampled rows: O {eo:.2e} LSE {el:.2e} dQ {edq:.2e}", flush=True)
+    assert eo <= O_TOL and el <= LSE_TOL and edq <= GRAD_TOL
+    return q, k, v, do
+
+
+def _check_keys(q, k, v, do, out, w, rng, max_len, n_pairs, label):
+    cu = w.cu_seqlens
+    lens = np.diff(cu)
+    cand = [b for b in range(len(lens)) if 0 < lens[b] <= max_len]
+    if not cand:
+        return
+    for b in rng.choice(cand, size=min(n_pairs, len(cand)), replace=False):
+        h = int(rng.integers(w.n_heads))
+        s0, s1 = int(cu[b]), int(cu[b + 1])
+        keys = np.unique(np.concatenate([[s0, s1 - 1], rng.integers(s0, s1, 62)]))
+        heads = np.full(keys.size, h)
+        rdk, rdv = A.attention_dkdv_rows(do, q, k, v, cu, w.scale, w.causal, keys, heads)
+        # scale: the largest gradient magnitude in this (sequence, head)
+        full_dk = I.bf16_to_f64(out["dk"][s0:s1, h])  # (sequence, head) slice only
+        full_dv = I.bf16_to_f64(out["dv"][s0:s1, h])
+        ek = float(np.max(np.abs(full_dk[keys - s0] - rdk)) / max(np.max(np.abs(rdk)), np.max(np.abs(full_dk))))
+        ev = float(np.max(np.abs(full_dv[keys - s0] - rdv)) / max(np.max(np.abs(rdv)), np.max(np.abs(full_dv))))
+        print(f"{label}: seq {b} (len {s1 - s0}) head {h}: dK {ek:.2e} dV {ev:.2e}", flush=True)
+        assert ek <= GRAD_TOL and ev <= GRAD_TOL
+
+
+def _check_identities(do, out, w, label):
+    """sum_j dV_j = sum_i dO_i and sum_j dK_j = 0 per (sequence, head)."""
+    cu = w.cu_seqlens
+    worst_v = worst_k = 0.0
+    for b in range(len(cu) - 1):
+        s0, s1 = int(cu[b]), int(cu[b + 1])
+        if s1 == s0:
+            continue
+        dk = I.bf16_to_f64(out["dk"][s0:s1])
+        dv = I.bf16_to_f64(out["dv"][s0:s1])
+        dob = np.asarray(do[s0:s1], dtype=np.float64)
+        # bf16 rounding of each summand bounds the error of the sums
+        bound_v = 2.0 ** -8 * np.abs(dv).sum(0) + 1e-6 * np.abs(dob).sum(0)
+        bound_k = 2.0 ** -8 * np.abs(dk).sum(0) + 1e-30
+        ev = np.abs(dv.sum(0) - dob.sum(0)) / bound_v
+        ek = np.abs(dk.sum(0)) / bound_k
+        worst_v, worst_k = max(worst_v, float(ev.max())), max(worst_k, float(ek.max()))
+    print(f"{label}: identity residual / rounding bound: dV {worst_v:.3f} dK {worst_k:.3f}", flush=True)
+    assert worst_v <= 1.0 and worst_k <= 1.0
+
+
+def test_video_short_mix_bench_batch(torch):
+    """32 clips of 1k..8k tokens, H16, D72: the exact batch bench.py times."""
+    rng = np.random.default_rng(0)
+    w = I.video_short_mix(rng)
+    bits, out = _run(torch, w, rng)
+    srng = np.random.default_rng(100)
+    q, k, v, do = _check_rows(bits, out, w, srng, 2048, "video short")
+    _check_keys(q, k, v, do, out, w, srng, 8192, 4, "video short")
+    _check_identities(do, out, w, "video short")
+
+
+def test_video_long_tail_pack(torch):
+    rng = np.random.default_rng(0)
+    w = I.video_long_tail_packs(rng, n_packs=1)[0]
+    bits, out = _run(torch, w, rng)
+    srng = np.random.default_rng(101)
+    q, k, v, do = _check_rows(bits, out, w, srng, 1024, "video long-tail")
+    _check_keys(q, k, v, do, out, w, srng, 8192, 3, "video long-tail")
+    _check_identities(do, out, w, "video long-tail")
+
+
+@pytest.mark.parametrize("length", [131072, 262144])
+def test_ulysses_shard(torch, length):
+    """One device's Ulysses shard: a single sequence, 2 heads, D128."""
+    rng = np.random.default_rng(0)
+    w = I.ulysses_shard(length)
+    bits, out = _run(torch, w, rng)
+    srng = np.random.default_rng(102)
+    q, k, v, do = _check_rows(bits, out, w, srng, 384, f"ulysses {length}")
+    _check_identities(do, out, w, f"ulysses {length}")
+
+
+def test_ulysses_shape_keys_at_16k(torch):
+    """Same launch configuration as the Ulysses shard (H2, D128, one
+    sequence) at a length whose key columns the oracle evaluates quickly."""
+    rng = np.random.default_rng(3)
+    w = I.Workload("ulysses-shaped 16k", [16384], 2, 128, False, 1 / math.sqrt(128))
+    bits, out = _run(torch, w, rng)
+    srng = np.random.default_rng(103)
+    q, k, v, do = _check_rows(bits, out, w, srng, 256, "16k")
+    _check_keys(q, k, v, do, out, w, srng, 16384, 1, "16k")
+
+
+def test_text_causal_pack(torch):
+    """Log-normal documents packed to 256k tokens, causal, H32, D128."""
+    rng = np.random.default_rng(0)
+    w = I.text_packs(rng, 1)[0]
+    bits, out = _run(torch, w, rng)
+    srng = np.random.default_rng(104)
+    q, k, v, do = _check_rows(bits, out, w, srng, 256, "text causal")
+    _check_keys(q, k, v, do, out, w, srng, 4096, 3, "text causal")
+    _check_identities(do, out, w, "text causal")

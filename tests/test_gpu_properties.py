@@ -1,0 +1,122 @@
+"""GPU properties that hold exactly: run-to-run bitwise determinism of every
+output, bitwise invariance of a sequence's outputs to its position in the
+pack, and the cost profiler feeding the planner."""
+
+import math
+
+import numpy as np
+import pytest
+
+from oracle import planner as O
+from paper_2608_07524_amd import inputs as I
+
+from gpu_util import to_bits, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    t = pytest.importorskip("torch")
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_07524_amd as P
+    P.load()
+    return t
+
+
+def _outputs(torch, bits, cu, scale, causal):
+    import paper_2608_07524_amd as P
+    q, k, v, do = (to_device(torch, b) for b in bits)
+    o, lse = P.varlen_attn_fwd(q, k, v, cu, scale, causal)
+    dq, dk, dv = P.varlen_attn_bwd(do, o, lse, q, k, v, cu, scale, causal)
+    torch.cuda.synchronize()
+    return [to_bits(o), lse.cpu().numpy(), to_bits(dq), to_bits(dk), to_bits(dv)]
+
+
+@pytest.mark.parametrize("D,causal", [(72, False), (128, True)])
+def test_bitwise_deterministic(torch, D, causal):
+    rng = np.random.default_rng(7)
+    lengths = [700, 1, 2049, 300]
+    cu = I.cu_from_lengths(lengths)
+    bits = I.tensors(rng, int(cu[-1]), 4, D)
+    a = _outputs(torch, bits, cu, 1 / math.sqrt(D), causal)
+    b = _outputs(torch, bits, cu, 1 / math.sqrt(D), causal)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_position_in_pack_invariance(torch, causal):
+    """A sequence's outputs do not depend on where it sits in the pack or
+    on its neighbours (no cross-sequence reads)."""
+    rng = np.random.default_rng(8)
+    H, D = 2, 72
+    target = I.tensors(rng, 333, H, D)
+    left = I.tensors(rng, 517, H, D)
+    right = I.tensors(rng, 64, H, D)
+    solo = _outputs(torch, target, [0, 333], 0.1, causal)
+    packed_bits = [np.concatenate([l, t, r]) for l, t, r in zip(left, target, right)]
+    packed = _outputs(torch, packed_bits, [0, 517, 850, 914], 0.1, causal)
+    sl = slice(517, 850)
+    for i, (x, y) in enumerate(zip(solo, packed)):
+        if i == 1:  # LSE is [H, T]
+            assert np.array_equal(x, y[:, sl])
+        else:
+            assert np.array_equal(x, y[sl])
+
+
+def test_profile_cost_rows(torch):
+    import paper_2608_07524_amd as P
+    lengths = [1024, 2048, 4096, 8192]
+    rows = P.profile_cost(lengths, n_heads=2, head_dim=128, warmup=2, reps=5, lin_f_ps_per_token=1000,
+                          act_bytes_per_token=34 * 256, inp_bytes_per_token=2 * 256)
+    for s, r in zip(lengths, rows):
+        print(f"profile s={s}: t_f {r.t_f_ns} ns t_b {r.t_b_ns} ns", flush=True)
+        assert r.seq_len == s and r.t_f_ns > 0 and r.t_b_ns > 0
+        assert r.m_bytes == 34 * 256 * s and r.m_inp_bytes == 2 * 256 * s
+        assert r.t_f_ns >= s  # the linear term alone is 1 ns per token
+    # quadratic attention cost: doubling the length at least doubles the time
+    for a, b in zip(rows, rows[1:]):
+        assert b.t_f_ns > 1.5 * a.t_f_ns and b.t_b_ns > 1.5 * a.t_b_ns
+    # a measured table plans bit-exactly against the integer oracle
+    table = O.CostTable([O.CostRow(r.seq_len, r.t_f_ns, r.t_b_ns, r.m_bytes, r.m_inp_bytes) for r in rows],
+                        28, 100_000, 900 << 20)
+    opts = O.PlanOpts(n_heads=16, hidden=1152)
+    seqs = [1000, 8000, 3000, 2048, 5000, 700]
+    ref = O.plan(seqs, table, 1 << 30, opts)
+    got = P.plan(seqs, rows, 28, 100_000, 900 << 20, 1 << 30, n_heads=16, hidden=1152)
+    assert (got.sp_size, got.micro_batch, got.grad_accum, got.recompute_layers) == \
+        (ref.sp_size, ref.micro_batch, ref.grad_accum, ref.recompute_layers)
+
+
+def test_text_lm_planning_over_1000_packs(torch):
+    """The text-LM workload: profile per-length causal costs at H32, D128,
+    then plan 1000 packs in groups of 8 (and 32): bit-exact with the oracle."""
+    import paper_2608_07524_amd as P
+    lengths = [2 ** e for e in range(7, 18)]
+    rows = P.profile_cost(lengths, n_heads=32, head_dim=128, causal=True, warmup=1, reps=3,
+                          act_bytes_per_token=34 * 4096, inp_bytes_per_token=2 * 4096)
+    table = O.CostTable([O.CostRow(r.seq_len, r.t_f_ns, r.t_b_ns, r.m_bytes, r.m_inp_bytes) for r in rows],
+                        42, 1_000_000, 20 << 30)
+    packs = I.text_packs(np.random.default_rng(0), 1000)
+    budget = 288 << 30
+    opts = O.PlanOpts(n_heads=32, hidden=4096, b_max=1)
+    for group in (8, 32):
+        for g0 in range(0, 1000, group):
+            batch = packs[g0:g0 + group]
+            seqs = [s for p in batch for s in p.lengths]
+            offs = np.concatenate([[0], np.cumsum([len(p.lengths) for p in batch])]).tolist()
+            try:
+                ref = O.plan(seqs, table, budget, opts, batch_offsets=offs)
+            except O.PlanError as e:
+                with pytest.raises(P.DCPError) as ei:
+                    P.plan(seqs, rows, 42, 1_000_000, 20 << 30, budget, batch_offsets=offs, n_heads=32,
+                           hidden=4096, b_max=1)
+                assert ei.value.code == e.code
+                continue
+            got = P.plan(seqs, rows, 42, 1_000_000, 20 << 30, budget, batch_offsets=offs, n_heads=32, hidden=4096,
+                         b_max=1)
+            for f in ("sp_size", "micro_batch", "grad_accum", "recompute_layers", "step_time_ns", "mem_bytes",
+                      "idle_ns", "makespan_ns"):
+                assert getattr(got, f) == getattr(ref, f), (g0, f)
