@@ -26,6 +26,8 @@
 //                                                       B = dS^T from registers)
 // The dQ pass recomputes S and dP (two extra products) instead of adding
 // per-key-tile partial dQ into an fp32 accumulator with atomics.
+#include <type_traits>
+
 #include "attn_common.h"
 #include "attn_launch.h"
 
@@ -116,26 +118,35 @@ template <int D, int NW, bool CAUSAL>
 __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
-    __bf16* __restrict__ dk, __bf16* __restrict__ dv, const WorkUnit* __restrict__ units, int H, int T, float scale,
+    __bf16* __restrict__ dk, __bf16* __restrict__ dv, const WorkUnit* __restrict__ units, int per_xcd, int H, int T, float scale,
     float scale_log2) {
   using S = BwdShape<D>;
-  constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR, QSTR = S::RSTR;
+  constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
+  // Q and dO are each kept twice per buffer: rows read 16 B per lane (A
+  // operands of S and dP) and rows read by transposing reads (B operands of
+  // dK and dV), each with its conflict-free stride.
+  constexpr int RSTR = S::DP + 8;
+  constexpr int TSTR = S::TSTR;
   constexpr int NT = 64 * NW;
   constexpr int BM = kBwdBM;  // queries per step
   constexpr int NCHQ = BM * CPR;
   constexpr int CPTQ = (NCHQ + NT - 1) / NT;
-  constexpr int QBUF = BM * QSTR;
+  constexpr int RBUF = BM * RSTR, TBUF = BM * TSTR;
+  constexpr int SLOT = 2 * RBUF + 2 * TBUF;  // one double-buffered tensor
+  constexpr int SSTR = S::RSTR;              // epilogue staging stride
 
-  // Q and dO tiles (double-buffered) in one array, so the epilogue can
-  // reuse the whole block as staging space.
-  __shared__ __attribute__((aligned(16))) __bf16 qdo_lds[4 * QBUF];
-  __bf16* const Qs = qdo_lds;
-  __bf16* const dOs = qdo_lds + 2 * QBUF;
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * SLOT];
+  __bf16* const Qr = lds;                    // [2][BM][RSTR]
+  __bf16* const Qt = lds + 2 * RBUF;         // [2][BM][TSTR]
+  __bf16* const dOr = lds + SLOT;
+  __bf16* const dOt = lds + SLOT + 2 * RBUF;
   __shared__ __attribute__((aligned(16))) float lse_s[2 * BM];
   __shared__ __attribute__((aligned(16))) float dlt_s[2 * BM];
+  static_assert(2 * SLOT >= NW * 32 * SSTR, "staging area too small");
 
-  const WorkUnit u = units[blockIdx.x];
-  const int h = blockIdx.y;
+  const WorkUnit u = unit_for_block(units, per_xcd);
+  if (u.rows == 0) return;
+  const int h = u.head;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -152,14 +163,22 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_kernel(
   const float* lseh = lse + int64_t(h) * T + u.seq0;
   const float* dlth = delta + int64_t(h) * T + u.seq0;
 
-  for (int i = tid; i < 2 * BM * (QSTR - D); i += NT) {
-    const int r = i / (QSTR - D), c = D + i % (QSTR - D);
-    Qs[r * QSTR + c] = __bf16(0.f);
-    dOs[r * QSTR + c] = __bf16(0.f);
+  // Pad columns are never written by tile loads; the contraction reads
+  // columns up to DP and the transposing reads up to NDB*32.
+  for (int i = tid; i < 2 * BM * (RSTR - D); i += NT) {
+    const int r = i / (RSTR - D), c = D + i % (RSTR - D);
+    Qr[r * RSTR + c] = __bf16(0.f);
+    dOr[r * RSTR + c] = __bf16(0.f);
+  }
+  for (int i = tid; i < 2 * BM * (TSTR - D); i += NT) {
+    const int r = i / (TSTR - D), c = D + i % (TSTR - D);
+    Qt[r * TSTR + c] = __bf16(0.f);
+    dOt[r * TSTR + c] = __bf16(0.f);
   }
 
   // K and V fragments (B operands of S = Q K^T and dP = dO V^T): lane (g, j)
-  // holds key j of this wavefront, columns 16*kd + 8*g .. +7.
+  // holds key j of this wavefront, columns 16*kd + 8*g .. +7.  Keys past the
+  // sequence end are zero; their dK, dV rows are never stored.
   const int my_key = 32 * wave + j;  // tile-relative
   const bool key_ok = my_key < u.rows;
   bf16x8 kf[NKD], vf[NKD];
@@ -209,8 +228,10 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_kernel(
       const int ch = tid + NT * c;
       if (NCHQ % NT == 0 || ch < NCHQ) {
         const int r = ch / CPR, cc = ch % CPR;
-        *reinterpret_cast<u32x4*>(&Qs[buf * QBUF + r * QSTR + cc * 8]) = qreg[c];
-        *reinterpret_cast<u32x4*>(&dOs[buf * QBUF + r * QSTR + cc * 8]) = doreg[c];
+        *reinterpret_cast<u32x4*>(&Qr[buf * RBUF + r * RSTR + cc * 8]) = qreg[c];
+        *reinterpret_cast<u32x4*>(&Qt[buf * TBUF + r * TSTR + cc * 8]) = qreg[c];
+        *reinterpret_cast<u32x4*>(&dOr[buf * RBUF + r * RSTR + cc * 8]) = doreg[c];
+        *reinterpret_cast<u32x4*>(&dOt[buf * TBUF + r * TSTR + cc * 8]) = doreg[c];
       }
     }
     if (tid < BM) {
@@ -236,70 +257,96 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_kernel(
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const int wave_key_lo = key_t0 + 32 * wave;  // smallest key of this wavefront
 
-  for (int it = 0; it < n_qt; ++it) {
-    const int buf = it & 1;
-    const int q0 = q_begin + it * BM;
-    if (it + 1 < n_qt) load_q_tile(q0 + BM);
-    const __bf16* Qb = &Qs[buf * QBUF];
-    const __bf16* dOb = &dOs[buf * QBUF];
+  // One 32-query block against this wavefront's 32 keys.  MASK applies the
+  // causal mask (only blocks crossing the diagonal need it).
+  auto process_block = [&](int buf, int q0, int qb, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    const __bf16* Qb = &Qr[buf * RBUF];
+    const __bf16* dOb = &dOr[buf * RBUF];
+    const __bf16* Qtb = &Qt[buf * TBUF];
+    const __bf16* dOtb = &dOt[buf * TBUF];
     const float* lseb = &lse_s[buf * BM];
     const float* dltb = &dlt_s[buf * BM];
-
+    f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
-    for (int qb = 0; qb < BM / 32; ++qb) {
-      // causal: a 32-query block entirely above this wavefront's keys adds nothing
-      if (CAUSAL && q0 + 32 * qb + 31 < wave_key_lo) continue;
-      f32x16 s = f32x16{}, dp = f32x16{};
+    for (int kd = 0; kd < NKD; ++kd) {
+      const bf16x8 aq = lds_read_b128(&Qb[(32 * qb + j) * RSTR + 16 * kd + 8 * g]);
+      s = mfma32(aq, kf[kd], s);
+      const bf16x8 ado = lds_read_b128(&dOb[(32 * qb + j) * RSTR + 16 * kd + 8 * g]);
+      dp = mfma32(ado, vf[kd], dp);
+    }
+    // This lane holds key `key_seq` against queries 32qb + 8b + 4g + c.
+    bf16x8 pa[2], da[2];
 #pragma unroll
-      for (int kd = 0; kd < NKD; ++kd) {
-        const bf16x8 aq = lds_read_b128(&Qb[(32 * qb + j) * QSTR + 16 * kd + 8 * g]);
-        s = mfma32(aq, kf[kd], s);
-        const bf16x8 ado = lds_read_b128(&dOb[(32 * qb + j) * QSTR + 16 * kd + 8 * g]);
-        dp = mfma32(ado, vf[kd], dp);
-      }
-      // This lane holds key `key_seq` against queries 32qb + 8b + 4g + c.
-      bf16x8 pa[2], da[2];
+    for (int b = 0; b < 4; ++b) {
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lseb[32 * qb + 8 * b + 4 * g]);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dltb[32 * qb + 8 * b + 4 * g]);
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lseb[32 * qb + 8 * b + 4 * g]);
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dltb[32 * qb + 8 * b + 4 * g]);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const int r = 4 * b + c;
-          float p = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -l4[c]));
-          if (CAUSAL && key_seq > q0 + 32 * qb + 8 * b + 4 * g + c) p = 0.f;
-          if (!key_ok) p = 0.f;
-          pa[b >> 1][4 * (b & 1) + c] = __bf16(p);
-          da[b >> 1][4 * (b & 1) + c] = __bf16(p * (dp[r] - d4[c]));
-        }
-      }
-      // dV += P^T dO and dK += dS^T Q: B = rows (queries) x columns (d),
-      // fetched column-wise with transposing reads.
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int off = (32 * qb + 16 * hh + 4 * g + tr_row) * QSTR + 32 * db + tr_col;
-          const bf16x8 bdo = cat(lds_read_tr(&dOb[off]), lds_read_tr(&dOb[off + 8 * QSTR]));
-          dv_acc[db] = mfma32(pa[hh], bdo, dv_acc[db]);
-          const bf16x8 bq = cat(lds_read_tr(&Qb[off]), lds_read_tr(&Qb[off + 8 * QSTR]));
-          dk_acc[db] = mfma32(da[hh], bq, dk_acc[db]);
-        }
+      for (int c = 0; c < 4; ++c) {
+        const int r = 4 * b + c;
+        float p = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -l4[c]));
+        if (MASK && key_seq > q0 + 32 * qb + 8 * b + 4 * g + c) p = 0.f;
+        pa[b >> 1][4 * (b & 1) + c] = __bf16(p);
+        da[b >> 1][4 * (b & 1) + c] = __bf16(p * (dp[r] - d4[c]));
       }
     }
-    if (it + 1 < n_qt) store_q_tile(buf ^ 1);
-    __syncthreads();
-  }
+    // dV += P^T dO and dK += dS^T Q: B = rows (queries) x columns (d),
+    // fetched column-wise with transposing reads.
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int off = (32 * qb + 16 * hh + 4 * g + tr_row) * TSTR + 32 * db + tr_col;
+        const bf16x8 bdo = cat(lds_read_tr(&dOtb[off]), lds_read_tr(&dOtb[off + 8 * TSTR]));
+        dv_acc[db] = mfma32(pa[hh], bdo, dv_acc[db]);
+        const bf16x8 bq = cat(lds_read_tr(&Qtb[off]), lds_read_tr(&Qtb[off + 8 * TSTR]));
+        dk_acc[db] = mfma32(da[hh], bq, dk_acc[db]);
+      }
+    }
+  };
 
-  // Epilogue through LDS (the Q / dO buffers are free now): each wavefront
+  // Query tiles are walked in two phases per wavefront: (causal only) those
+  // crossing its diagonal, where blocks entirely above its keys are skipped
+  // and the rest masked, then those needing no mask.  Both phases run the
+  // same load / store / barrier sequence.
+  auto run = [&](int it0, int it1, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    for (int it = it0; it < it1; ++it) {
+      const int buf = it & 1;
+      const int q0 = q_begin + it * BM;
+      if (it + 1 < n_qt) load_q_tile(q0 + BM);
+#pragma unroll
+      for (int qb = 0; qb < BM / 32; ++qb) {
+        if (MASK) {
+          const int qa = q0 + 32 * qb;
+          if (qa + 31 < wave_key_lo) continue;  // every query precedes every key
+          if (qa >= wave_key_lo + 31) {
+            process_block(buf, q0, qb, std::false_type{});
+            continue;
+          }
+        }
+        process_block(buf, q0, qb, std::integral_constant<bool, MASK>{});
+      }
+      if (it + 1 < n_qt) store_q_tile(buf ^ 1);
+      __syncthreads();
+    }
+  };
+  int it_plain = 0;
+  if (CAUSAL) {
+    // first step whose queries all follow all of this wavefront's keys
+    it_plain = min(n_qt, max(0, (wave_key_lo + 31 - q_begin + BM - 1) / BM));
+    run(0, it_plain, std::true_type{});
+  }
+  run(it_plain, n_qt, std::false_type{});
+
+  // Epilogue through LDS (the tile buffers are free now): each wavefront
   // stages its 32 rows of dK, then of dV.
-  static_assert(4 * QBUF >= NW * 32 * QSTR, "staging area too small");
-  __bf16* stage = qdo_lds + wave * 32 * QSTR;  // 32 rows per wavefront
+  __bf16* stage = lds + wave * 32 * SSTR;  // 32 rows per wavefront
   const int n_rows = max(0, min(32, u.rows - 32 * wave));
   __bf16* dk_base = dk + int64_t(u.row0 + 32 * wave) * ts + int64_t(h) * D;
   __bf16* dv_base = dv + int64_t(u.row0 + 32 * wave) * ts + int64_t(h) * D;
-  store_rows_bf16<D, NDB>(dk_acc, scale, stage, QSTR, dk_base, ts, n_rows, lane);
-  store_rows_bf16<D, NDB>(dv_acc, 1.f, stage, QSTR, dv_base, ts, n_rows, lane);
+  store_rows_bf16<D, NDB>(dk_acc, scale, stage, SSTR, dk_base, ts, n_rows, lane);
+  store_rows_bf16<D, NDB>(dv_acc, 1.f, stage, SSTR, dv_base, ts, n_rows, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -308,7 +355,7 @@ template <int D, int NW, bool CAUSAL>
 __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
-    __bf16* __restrict__ dq, const WorkUnit* __restrict__ units, int H, int T, float scale, float scale_log2) {
+    __bf16* __restrict__ dq, const WorkUnit* __restrict__ units, int per_xcd, int H, int T, float scale, float scale_log2) {
   using S = BwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
   constexpr int KSTR = S::DP + 8;  // K and V rows read 16 B per lane
@@ -323,8 +370,9 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   __shared__ __attribute__((aligned(16))) __bf16 Vs[2 * KBUF];
   __shared__ __attribute__((aligned(16))) __bf16 Kt[2 * TBUF];
 
-  const WorkUnit u = units[blockIdx.x];
-  const int h = blockIdx.y;
+  const WorkUnit u = unit_for_block(units, per_xcd);
+  if (u.rows == 0) return;
+  const int h = u.head;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -417,58 +465,76 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const int wave_last_q = wave_q0 + 31;
 
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < n_tiles) load_tile(kt + 1);
-    const int k0 = kt * BN;
-    if (!CAUSAL || k0 <= wave_last_q) {
-      const __bf16* Kb = &Ks[buf * KBUF];
-      const __bf16* Vb = &Vs[buf * KBUF];
-      const __bf16* Tb = &Kt[buf * TBUF];
-      f32x16 s[BN / 32], dp[BN / 32];
+  // One key tile against this wavefront's 32 queries.  MASK covers tiles
+  // crossing the sequence end or the causal diagonal.
+  auto process_tile = [&](int buf, int k0, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    const __bf16* Kb = &Ks[buf * KBUF];
+    const __bf16* Vb = &Vs[buf * KBUF];
+    const __bf16* Tb = &Kt[buf * TBUF];
+    f32x16 s[BN / 32], dp[BN / 32];
+#pragma unroll
+    for (int kb = 0; kb < BN / 32; ++kb) {
+      s[kb] = f32x16{};
+      dp[kb] = f32x16{};
+    }
+#pragma unroll
+    for (int kd = 0; kd < NKD; ++kd) {
 #pragma unroll
       for (int kb = 0; kb < BN / 32; ++kb) {
-        s[kb] = f32x16{};
-        dp[kb] = f32x16{};
+        const bf16x8 ak = lds_read_b128(&Kb[(32 * kb + j) * KSTR + 16 * kd + 8 * g]);
+        s[kb] = mfma32(ak, qf[kd], s[kb]);
+        const bf16x8 av = lds_read_b128(&Vb[(32 * kb + j) * KSTR + 16 * kd + 8 * g]);
+        dp[kb] = mfma32(av, df[kd], dp[kb]);
       }
+    }
+    bf16x8 dsb[BN / 32][2];
 #pragma unroll
-      for (int kd = 0; kd < NKD; ++kd) {
+    for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
-        for (int kb = 0; kb < BN / 32; ++kb) {
-          const bf16x8 ak = lds_read_b128(&Kb[(32 * kb + j) * KSTR + 16 * kd + 8 * g]);
-          s[kb] = mfma32(ak, qf[kd], s[kb]);
-          const bf16x8 av = lds_read_b128(&Vb[(32 * kb + j) * KSTR + 16 * kd + 8 * g]);
-          dp[kb] = mfma32(av, df[kd], dp[kb]);
+      for (int r = 0; r < 16; ++r) {
+        float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], scale_log2, -lse2));
+        if constexpr (MASK) {
+          const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * g + (r & 3);
+          if (key >= seqlen || (CAUSAL && key > my_q)) p = 0.f;
         }
+        dsb[kb][r >> 3][r & 7] = __bf16(p * (dp[kb][r] - dlt));
       }
-      const bool need_mask = (k0 + BN > seqlen) || (CAUSAL && k0 + BN - 1 > wave_q0);
-      bf16x8 dsb[BN / 32][2];
+    // dQ^T += K^T dS^T: A = K^T (rows d, keys 32kb + 16hh + 4g + {0..3, 8..11}).
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], scale_log2, -lse2));
-          if (need_mask) {
-            const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * g + (r & 3);
-            if (key >= seqlen || (CAUSAL && key > my_q)) p = 0.f;
-          }
-          dsb[kb][r >> 3][r & 7] = __bf16(p * (dp[kb][r] - dlt));
+        for (int hh = 0; hh < 2; ++hh) {
+          const __bf16* p = &Tb[(32 * kb + 16 * hh + 4 * g + tr_row) * TSTR + 32 * db + tr_col];
+          const bf16x8 a = cat(lds_read_tr(p), lds_read_tr(p + 8 * TSTR));
+          acc[db] = mfma32(a, dsb[kb][hh], acc[db]);
         }
-      // dQ^T += K^T dS^T: A = K^T (rows d, keys 32kb + 16hh + 4g + {0..3, 8..11}).
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int kb = 0; kb < BN / 32; ++kb)
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const __bf16* p = &Tb[(32 * kb + 16 * hh + 4 * g + tr_row) * TSTR + 32 * db + tr_col];
-            const bf16x8 a = cat(lds_read_tr(p), lds_read_tr(p + 8 * TSTR));
-            acc[db] = mfma32(a, dsb[kb][hh], acc[db]);
-          }
-    }
-    if (kt + 1 < n_tiles) store_tile(buf ^ 1);
-    __syncthreads();
+  };
+
+  // Key tiles in up to three phases per wavefront (unmasked, masked, idle),
+  // each with the same load / store / barrier sequence.
+  int t_mask = min(n_tiles, seqlen / BN);
+  int t_idle = n_tiles;
+  if (CAUSAL) {
+    t_mask = min(t_mask, (wave_q0 + 1) / BN);
+    t_idle = min(n_tiles, wave_last_q / BN + 1);
   }
+  auto run = [&](int kt0, int kt1, auto mode_tag) {
+    constexpr int MODE = decltype(mode_tag)::value;  // 0 unmasked, 1 masked, 2 idle
+    for (int kt = kt0; kt < kt1; ++kt) {
+      const int buf = kt & 1;
+      if (kt + 1 < n_tiles) load_tile(kt + 1);
+      if constexpr (MODE == 0) process_tile(buf, kt * BN, std::false_type{});
+      if constexpr (MODE == 1) process_tile(buf, kt * BN, std::true_type{});
+      if (kt + 1 < n_tiles) store_tile(buf ^ 1);
+      __syncthreads();
+    }
+  };
+  run(0, t_mask, std::integral_constant<int, 0>{});
+  run(t_mask, t_idle, std::integral_constant<int, 1>{});
+  if (CAUSAL) run(t_idle, n_tiles, std::integral_constant<int, 2>{});
 
   // Epilogue: lane (g, j) holds query j, columns 32db + 8rb + 4g + {0..3}.
   if (q_ok) {
@@ -503,22 +569,22 @@ hipError_t launch_bwd_t(const BwdArgs& a) {
   if (a.n_units > 0) {
     if (ev.begin) (void)hipEventRecord(ev.begin, a.stream);
     constexpr int NW = bwd_dkdv_waves(D);
-    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, NW, CAUSAL>), dim3(a.n_units, a.n_heads), dim3(64 * NW), 0,
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, NW, CAUSAL>), dim3(a.n_units), dim3(64 * NW), 0,
                        a.stream, static_cast<const __bf16*>(a.q),
                        static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
                        static_cast<const __bf16*>(a.dout), a.lse, a.delta, static_cast<__bf16*>(a.dk),
-                       static_cast<__bf16*>(a.dv), static_cast<const WorkUnit*>(a.units), a.n_heads,
+                       static_cast<__bf16*>(a.dv), static_cast<const WorkUnit*>(a.units), a.n_units / kNumXcd, a.n_heads,
                        a.total_tokens, a.scale, a.scale * kLog2e);
     hipError_t e = hipGetLastError();
     if (ev.end) (void)hipEventRecord(ev.end, a.stream);
     if (e != hipSuccess) return e;
   }
   if (a.n_qunits > 0) {
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, kBwdDqWaves, CAUSAL>), dim3(a.n_qunits, a.n_heads),
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, kBwdDqWaves, CAUSAL>), dim3(a.n_qunits),
                        dim3(64 * kBwdDqWaves), 0, a.stream, static_cast<const __bf16*>(a.q),
                        static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
                        static_cast<const __bf16*>(a.dout), a.lse, a.delta, static_cast<__bf16*>(a.dq),
-                       static_cast<const WorkUnit*>(a.qunits), a.n_heads, a.total_tokens, a.scale,
+                       static_cast<const WorkUnit*>(a.qunits), a.n_qunits / kNumXcd, a.n_heads, a.total_tokens, a.scale,
                        a.scale * kLog2e);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

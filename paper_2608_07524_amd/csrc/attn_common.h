@@ -24,14 +24,27 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// One tile of work: rows [row0, row0 + rows) of the packed tensor, all in
-// the sequence that occupies rows [seq0, seq0 + seqlen).
+// One tile of work: rows [row0, row0 + rows) of the packed tensor for head
+// `head`, all in the sequence that occupies rows [seq0, seq0 + seqlen).
+// rows == 0 marks padding (the workgroup exits at once).
 struct WorkUnit {
   int32_t row0;
   int32_t rows;
   int32_t seq0;
   int32_t seqlen;
+  int32_t head;
+  int32_t pad[3];
 };
+
+constexpr int kNumXcd = 8;  // MI355X: 8 accelerator dies, each with its own L2
+
+// The dispatcher hands workgroup i to die i % 8.  Work lists are laid out
+// as 8 consecutive per-die lists of `per_xcd` entries, so a die walks its
+// own list in order and tiles that share K/V (or Q/dO) meet in its L2.
+__device__ __forceinline__ const WorkUnit& unit_for_block(const WorkUnit* units, int per_xcd) {
+  const int i = blockIdx.x;
+  return units[(i % kNumXcd) * per_xcd + i / kNumXcd];
+}
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -68,8 +81,75 @@ __device__ __forceinline__ bf16x8 cat(const bf16x4& lo, const bf16x4& hi) {
 
 __device__ __forceinline__ bf16x8 lds_read_b128(const __bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
-__device__ __forceinline__ void atomic_add_f32(float* p, float v) {
-  __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Waits until at most N vector-memory operations of this wavefront are in
+// flight (gfx9 s_waitcnt: vmcnt split over bits 3:0 and 15:14; expcnt and
+// lgkmcnt left at their maxima, i.e. not waited on).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
 }
+
+// Direct global -> LDS copy of one ROWS-row tile (gfx950
+// global_load_lds_dwordx4: each lane moves 16 bytes, a wavefront fills 64
+// consecutive 16-byte LDS slots, no registers involved).  In LDS, slot
+// (r, c) of the tile sits at byte 16*(r*CPR_PAD + c); slots c < CPR_DATA of
+// rows r < valid_rows come from src + r*row_stride + 8c, slot c == CPR_DATA
+// from `first_pad` (a 16-byte constant chunk, e.g. [1, 0, ..., 0] for a
+// row-sum column) and every other slot from `zero`.  Every wavefront issues
+// exactly NI instructions per tile (the last one repeated when the tile
+// does not split evenly; the repeat rewrites identical bytes), so a fixed
+// wait_vmcnt count covers the tile on every wavefront.  Completion is
+// tracked by vmcnt only: wait, then barrier, before reading the tile.
+template <int ROWS, int CPR_PAD, int CPR_DATA, int NW>
+struct DmaTile {
+  static constexpr int NSLOT = ROWS * CPR_PAD;
+  static constexpr int NINS = NSLOT / 64;
+  static constexpr int NI = (NINS + NW - 1) / NW;
+  static_assert(NSLOT % 64 == 0, "tile must fill whole wavefront copies");
+  static_assert(CPR_DATA < CPR_PAD, "pad slots hold the constant chunks");
+
+  __device__ __forceinline__ static void issue(__bf16* lds_tile, const __bf16* src, int64_t row_stride,
+                                               int valid_rows, const __bf16* zero, const __bf16* first_pad,
+                                               int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int t = min(wave + NW * i, NINS - 1);
+      const int slot = 64 * t + lane;
+      const int r = slot / CPR_PAD, c = slot % CPR_PAD;
+      const __bf16* g = zero;
+      if (c < CPR_DATA) {
+        if (r < valid_rows) g = src + int64_t(r) * row_stride + 8 * c;
+      } else if (c == CPR_DATA) {
+        g = first_pad;
+      }
+      dma16(g, lds_tile + 512 * t);
+    }
+  }
+
+  // One global_load_lds_dwordx4: lane i's 16 bytes at `g` land in LDS at
+  // `lds_base` + 16*i.  Written as inline assembly: the compiler would
+  // otherwise treat the copy as possibly aliasing every LDS read and wait
+  // for it right away, which defeats copying ahead.  The callers' explicit
+  // vmcnt waits and barriers order it instead; callers also settle their
+  // own earlier vector loads before the first copy, so that no wait the
+  // compiler inserts later stands for a load it tracks.  M0 is written here
+  // and used by nothing else in these kernels (checked in the generated
+  // code: no other M0 reader).
+  __device__ __forceinline__ static void dma16(const __bf16* g, __bf16* lds_base) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane(
+        static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds_base)));  // low 32 bits = LDS offset
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(m0), "v"(reinterpret_cast<uint64_t>(g))
+                 : "memory");
+  }
+};
+
+// Offsets (bf16 elements) of the 16-byte constant chunks every attention
+// workspace starts with.
+constexpr int kConstZero = 0;   // [0, 0, 0, 0, 0, 0, 0, 0]
+constexpr int kConstOnes = 8;   // [1, 0, 0, 0, 0, 0, 0, 0]
+constexpr int kConstBytes = 256;
 
 }  // namespace dcp

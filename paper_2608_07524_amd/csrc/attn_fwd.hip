@@ -7,9 +7,8 @@
 // sequence only, so no off-diagonal (cross-sequence) block is ever touched.
 // NW wavefronts per workgroup, each owning 32*NQB query rows.
 //
-// Per key tile of BN = 64 keys (double-buffered in LDS; the next tile is
-// prefetched into registers while the current one is consumed, so there is
-// one barrier per tile):
+// Per key tile of BN = 64 keys (a three-stage LDS ring filled by direct
+// global-to-LDS copies two tiles ahead; one barrier per tile):
 //   S^T = K Q^T      A = K rows from LDS, B = Q rows kept in registers;
 //                    each lane ends up holding one query and 16 keys.
 //   m, P             row max: in-lane over 32 keys + one cross-half swap;
@@ -23,6 +22,8 @@
 // row in the last 32-row block of O^T (D = 72), a column of ones appended to
 // V makes the matrix cores produce the row sum l = sum_j P_ij as well.
 // Epilogue: O = O^T / l (bf16), LSE = (m + log2 l) * ln 2.
+#include <type_traits>
+
 #include "attn_common.h"
 #include "attn_launch.h"
 
@@ -52,22 +53,26 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
                                                            const __bf16* __restrict__ k,
                                                            const __bf16* __restrict__ v, __bf16* __restrict__ o,
                                                            float* __restrict__ lse,
-                                                           const WorkUnit* __restrict__ units, int H, int T,
+                                                           const __bf16* __restrict__ consts,
+                                                           const WorkUnit* __restrict__ units, int per_xcd, int H, int T,
                                                            float scale_log2) {
   using S = FwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, KSTR = S::KSTR, VSTR = S::VSTR, CPR = S::CPR;
   constexpr int BN = kFwdBN;
   constexpr int NT = 64 * NW;  // threads
   constexpr int QPW = 32 * NQB;
-  constexpr int NCH = BN * CPR;
-  constexpr int CPT = (NCH + NT - 1) / NT;
   constexpr int KBUF = BN * KSTR, VBUF = BN * VSTR;
+  using DK = DmaTile<BN, KSTR / 8, CPR, NW>;
+  using DV = DmaTile<BN, VSTR / 8, CPR, NW>;
+  constexpr int NI = DK::NI + DV::NI;  // copies per wavefront per tile
 
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[2 * KBUF];
-  __shared__ __attribute__((aligned(16))) __bf16 Vs[2 * VBUF];
+  // Three-stage ring: tile kt+2 streams in while tile kt is consumed.
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[3 * KBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[3 * VBUF];
 
-  const WorkUnit u = units[blockIdx.x];
-  const int h = blockIdx.y;
+  const WorkUnit u = unit_for_block(units, per_xcd);
+  if (u.rows == 0) return;
+  const int h = u.head;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -78,18 +83,10 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   const __bf16* qh = q + int64_t(u.seq0) * ts + int64_t(h) * D;
   const __bf16* kh = k + int64_t(u.seq0) * ts + int64_t(h) * D;
   const __bf16* vh = v + int64_t(u.seq0) * ts + int64_t(h) * D;
-
-  // Columns past D are never written by tile loads.  K pads must be zero
-  // (they enter the contraction); V pads are zero except column D, which
-  // holds ones when it is the row-sum column.
-  for (int i = tid; i < 2 * BN * (KSTR - D); i += NT) {
-    const int r = i / (KSTR - D), c = D + i % (KSTR - D);
-    Ks[r * KSTR + c] = __bf16(0.f);
-  }
-  for (int i = tid; i < 2 * BN * (VSTR - D); i += NT) {
-    const int r = i / (VSTR - D), c = D + i % (VSTR - D);
-    Vs[r * VSTR + c] = __bf16((S::ONES_ROW && c == D) ? 1.f : 0.f);
-  }
+  const __bf16* zero = consts + kConstZero;
+  // K pad columns must be zero (they enter the contraction); V's first pad
+  // column holds ones when it is the row-sum column.
+  const __bf16* v_pad = S::ONES_ROW ? consts + kConstOnes : zero;
 
   const int tile_q0 = u.row0 - u.seq0;       // first query of the tile, sequence-relative
   const int wave_q0 = tile_q0 + wave * QPW;  // first query of this wave
@@ -112,36 +109,27 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
     }
   }
 
+  // Settle the Q loads here: the tile copies below are invisible to the
+  // compiler's wait tracking, so no later compiler-inserted wait may stand
+  // for these loads inside the tile loop.
+  wait_vmcnt<0>();
+
   const int key_end = CAUSAL ? min(seqlen, tile_q0 + u.rows) : seqlen;
   const int n_tiles = (key_end + BN - 1) / BN;
 
-  u32x4 kreg[CPT], vreg[CPT];
-  auto load_tile = [&](int kt) {
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int ch = tid + NT * c;
-      if (NCH % NT == 0 || ch < NCH) {
-        const int r = ch / CPR, cc = ch % CPR;
-        const int key = kt * BN + r;
-        if (key < seqlen) {
-          kreg[c] = *reinterpret_cast<const u32x4*>(kh + int64_t(key) * ts + cc * 8);
-          vreg[c] = *reinterpret_cast<const u32x4*>(vh + int64_t(key) * ts + cc * 8);
-        } else {
-          kreg[c] = u32x4{0, 0, 0, 0};
-          vreg[c] = u32x4{0, 0, 0, 0};
-        }
-      }
-    }
+  auto issue_tile = [&](int kt) {
+    const int st = kt % 3;
+    const int valid = min(BN, seqlen - kt * BN);
+    DK::issue(&Ks[st * KBUF], kh + int64_t(kt) * BN * ts, ts, valid, zero, zero, wave, lane);
+    DV::issue(&Vs[st * VBUF], vh + int64_t(kt) * BN * ts, ts, valid, zero, v_pad, wave, lane);
   };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int ch = tid + NT * c;
-      if (NCH % NT == 0 || ch < NCH) {
-        const int r = ch / CPR, cc = ch % CPR;
-        *reinterpret_cast<u32x4*>(&Ks[buf * KBUF + r * KSTR + cc * 8]) = kreg[c];
-        *reinterpret_cast<u32x4*>(&Vs[buf * VBUF + r * VSTR + cc * 8]) = vreg[c];
-      }
+  // Before the barrier that ends tile kt: tile kt+1 must have landed; only
+  // tile kt+2's copies (issued this iteration) may still be in flight.
+  auto wait_next = [&](int kt) {
+    if (kt + 2 < n_tiles) {
+      wait_vmcnt<NI>();
+    } else {
+      wait_vmcnt<0>();
     }
   };
 
@@ -155,117 +143,138 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
     for (int db = 0; db < NDB; ++db) oacc[qb][db] = f32x16{};
   }
 
-  if (n_tiles > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
+  if (n_tiles > 0) issue_tile(0);
+  if (n_tiles > 1) issue_tile(1);
+  wait_next(-1);
   __syncthreads();
 
   const int wave_last_q = wave_q0 + QPW - 1;
-  // transposing-read addressing (see lds_read_tr): row and column offsets
-  const int tr_row = (lane & 15) >> 2;
-  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  // transposing-read addressing (see lds_read_tr): this lane's element
+  // offset inside a V tile; every other term is a compile-time constant
+  const int tr_off = (4 * g + ((lane & 15) >> 2)) * VSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  // and the 16-byte read offset inside a K tile
+  const int kr_off = j * KSTR + 8 * g;
 
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < n_tiles) load_tile(kt + 1);
-    const int k0 = kt * BN;
-    const bool active = !CAUSAL || k0 <= wave_last_q;
-    if (active) {
-      const __bf16* Kb = &Ks[buf * KBUF];
-      const __bf16* Vb = &Vs[buf * VBUF];
-      f32x16 s[2][NQB];
+  // One key tile.  MASK selects the variant for tiles that reach past the
+  // sequence end or cross the causal diagonal; it is a compile-time flag so
+  // the common unmasked tiles carry no per-element compare and select.
+  auto process_tile = [&](const __bf16* Kb, const __bf16* Vb, int k0, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    f32x16 s[2][NQB];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = f32x16{};
+#pragma unroll
+    for (int kd = 0; kd < NKD; ++kd) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const bf16x8 a = lds_read_b128(Kb + kr_off + 32 * kb * KSTR + 16 * kd);
+#pragma unroll
+        for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = mfma32(a, qf[qb][kd], s[kb][qb]);
+      }
+    }
+    if constexpr (MASK) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = f32x16{};
-#pragma unroll
-      for (int kd = 0; kd < NKD; ++kd) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          const bf16x8 a = lds_read_b128(&Kb[(32 * kb + j) * KSTR + 16 * kd + 8 * g]);
-#pragma unroll
-          for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = mfma32(a, qf[qb][kd], s[kb][qb]);
-        }
-      }
-      const bool need_mask = (k0 + BN > seqlen) || (CAUSAL && k0 + BN - 1 > wave_q0);
-      if (need_mask) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int qb = 0; qb < NQB; ++qb) {
-            const int qi = wave_q0 + 32 * qb + j;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * g + (r & 3);
-              if (key >= seqlen || (CAUSAL && key > qi)) s[kb][qb][r] = -INFINITY;
-            }
-          }
-      }
-      // Lazy rescale: move m only when a row's max outgrows it by > 2^8.
-      float mx[NQB];
-      bool grow = false;
-#pragma unroll
-      for (int qb = 0; qb < NQB; ++qb) {
-        float t = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) t = fmaxf(t, s[kb][qb][r]);
-        mx[qb] = half_swap_max(t) * scale_log2;
-        grow |= mx[qb] > m_use[qb] + kRescaleSlack;
-      }
-      if (__builtin_amdgcn_ballot_w64(grow)) {
-#pragma unroll
         for (int qb = 0; qb < NQB; ++qb) {
-          const float m_new = fmaxf(m_use[qb], mx[qb]);
-          const float alpha = __builtin_amdgcn_exp2f(m_use[qb] - m_new);  // 0 on the first tile
-          m_use[qb] = m_new;
-          l_run[qb] *= alpha;
-#pragma unroll
-          for (int db = 0; db < NDB; ++db) oacc[qb][db] *= alpha;
-        }
-      }
-      bf16x8 pb[2][2][NQB];
-#pragma unroll
-      for (int qb = 0; qb < NQB; ++qb) {
-        // every row has a finite max after its first tile (key 0 is visible)
-        const float mneg = -m_use[qb];
-        float lsum = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+          const int qi = wave_q0 + 32 * qb + j;
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][qb][r], scale_log2, mneg));
-            s[kb][qb][r] = p;
-            if (!S::ONES_ROW) lsum += p;
+            const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * g + (r & 3);
+            if (key >= seqlen || (CAUSAL && key > qi)) s[kb][qb][r] = -INFINITY;
           }
-        if (!S::ONES_ROW) l_run[qb] += lsum;
+        }
+    }
+    // Lazy rescale: move m only when a row's max outgrows it by > 2^8.
+    float mx[NQB];
+    bool grow = false;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+    for (int qb = 0; qb < NQB; ++qb) {
+      float t = -INFINITY;
 #pragma unroll
-          for (int hh = 0; hh < 2; ++hh)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) pb[kb][hh][qb][e] = __bf16(s[kb][qb][8 * hh + e]);
+        for (int r = 0; r < 16; ++r) t = fmaxf(t, s[kb][qb][r]);
+      mx[qb] = half_swap_max(t) * scale_log2;
+      grow |= mx[qb] > m_use[qb] + kRescaleSlack;
+    }
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+      for (int qb = 0; qb < NQB; ++qb) {
+        const float m_new = fmaxf(m_use[qb], mx[qb]);
+        const float alpha = __builtin_amdgcn_exp2f(m_use[qb] - m_new);  // 0 on the first tile
+        m_use[qb] = m_new;
+        l_run[qb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) oacc[qb][db] *= alpha;
       }
+    }
+    bf16x8 pb[2][2][NQB];
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
+    for (int qb = 0; qb < NQB; ++qb) {
+      // every row has a finite max after its first tile (key 0 is visible)
+      const float mneg = -m_use[qb];
+      float lsum = 0.f;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            // keys 32kb + 16hh + 4g + {0..3} and + 8 + {0..3}; column 32db + (lane % 32)
-            const __bf16* p = &Vb[(32 * kb + 16 * hh + 4 * g + tr_row) * VSTR + 32 * db + tr_col];
-            const bf16x8 a = cat(lds_read_tr(p), lds_read_tr(p + 8 * VSTR));
+        for (int r = 0; r < 16; ++r) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][qb][r], scale_log2, mneg));
+          s[kb][qb][r] = p;
+          if (!S::ONES_ROW) lsum += p;
+        }
+      if (!S::ONES_ROW) l_run[qb] += lsum;
 #pragma unroll
-            for (int qb = 0; qb < NQB; ++qb) oacc[qb][db] = mfma32(a, pb[kb][hh][qb], oacc[qb][db]);
-          }
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pb[kb][hh][qb][e] = __bf16(s[kb][qb][8 * hh + e]);
+    }
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          // keys 32kb + 16hh + 4g + {0..3} and + 8 + {0..3}; column 32db + (lane % 32)
+          const __bf16* p = Vb + tr_off + (32 * kb + 16 * hh) * VSTR + 32 * db;
+          const bf16x8 a = cat(lds_read_tr(p), lds_read_tr(p + 8 * VSTR));
+#pragma unroll
+          for (int qb = 0; qb < NQB; ++qb) oacc[qb][db] = mfma32(a, pb[kb][hh][qb], oacc[qb][db]);
         }
       }
     }
-    if (kt + 1 < n_tiles) store_tile(buf ^ 1);
-    __syncthreads();
+  };
+
+  // Each wavefront walks the key tiles in up to three phases: tiles that
+  // need no mask, the (at most two) tiles crossing the sequence end or its
+  // causal diagonal, and, when causal, tiles entirely above its queries.
+  // Every phase runs the same copy / wait / barrier sequence, so all
+  // wavefronts meet the same number of barriers.
+  const int n_full = seqlen / BN;  // tiles lying entirely inside the sequence
+  int t_mask = min(n_tiles, n_full);
+  int t_idle = n_tiles;
+  if (CAUSAL) {
+    t_mask = min(t_mask, (wave_q0 + 1) / BN);  // tiles whose last key is <= the wave's first query
+    t_idle = min(n_tiles, wave_last_q / BN + 1);
   }
+  auto run = [&](int kt0, int kt1, auto mode_tag) {
+    constexpr int MODE = decltype(mode_tag)::value;  // 0 unmasked, 1 masked, 2 idle
+    for (int kt = kt0; kt < kt1; ++kt) {
+      const int st = kt % 3;
+      if (kt + 2 < n_tiles) issue_tile(kt + 2);
+      if constexpr (MODE == 0) process_tile(&Ks[st * KBUF], &Vs[st * VBUF], kt * BN, std::false_type{});
+      if constexpr (MODE == 1) process_tile(&Ks[st * KBUF], &Vs[st * VBUF], kt * BN, std::true_type{});
+      wait_next(kt);
+      __syncthreads();
+    }
+  };
+  run(0, t_mask, std::integral_constant<int, 0>{});
+  run(t_mask, t_idle, std::integral_constant<int, 1>{});
+  if (CAUSAL) run(t_idle, n_tiles, std::integral_constant<int, 2>{});
 
   // Epilogue.
 #pragma unroll
@@ -306,13 +315,15 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
 
 template <int D, int NQB, int NW, bool CAUSAL>
 hipError_t launch_fwd_t(const FwdArgs& a) {
-  dim3 grid(a.n_units, a.n_heads);
+  dim3 grid(a.n_units);
   const KernelEvents& ev = kernel_events();
   if (ev.begin) (void)hipEventRecord(ev.begin, a.stream);
   hipLaunchKernelGGL((attn_fwd_kernel<D, NQB, NW, CAUSAL>), grid, dim3(64 * NW), 0, a.stream,
                      static_cast<const __bf16*>(a.q), static_cast<const __bf16*>(a.k),
                      static_cast<const __bf16*>(a.v), static_cast<__bf16*>(a.o), a.lse,
-                     static_cast<const WorkUnit*>(a.units), a.n_heads, a.total_tokens, a.scale * kLog2e);
+                     static_cast<const __bf16*>(a.consts), static_cast<const WorkUnit*>(a.units),
+                     a.n_units / kNumXcd, a.n_heads, a.total_tokens,
+                     a.scale * kLog2e);
   hipError_t e = hipGetLastError();
   if (ev.end) (void)hipEventRecord(ev.end, a.stream);
   return e;

@@ -24,8 +24,14 @@ constexpr int kFwdWaves = DCP_FWD_WAVES;
 #ifndef DCP_BWD_WAVES_D128
 #define DCP_BWD_WAVES_D128 4
 #endif
-constexpr int bwd_dkdv_waves(int head_dim) { return head_dim > 96 ? DCP_BWD_WAVES_D128 : 8; }
-constexpr int kBwdDqWaves = 8;
+#ifndef DCP_BWD_WAVES
+#define DCP_BWD_WAVES 8
+#endif
+#ifndef DCP_BWD_DQ_WAVES
+#define DCP_BWD_DQ_WAVES 8
+#endif
+constexpr int bwd_dkdv_waves(int head_dim) { return head_dim > 96 ? DCP_BWD_WAVES_D128 : DCP_BWD_WAVES; }
+constexpr int kBwdDqWaves = DCP_BWD_DQ_WAVES;
 constexpr int kBwdBM = 64;
 constexpr int kBwdDqBN = 64;
 
@@ -35,7 +41,8 @@ struct FwdArgs {
   const void* v;
   void* o;
   float* lse;
-  const void* units;  // device WorkUnit[n_units]
+  const void* consts;  // device: the 16-byte constant chunks (workspace head)
+  const void* units;   // device WorkUnit[n_units], 8 per-die lists of n_units / 8
   int n_units;
   int n_heads;
   int head_dim;
@@ -56,9 +63,9 @@ struct BwdArgs {
   void* dk;
   void* dv;
   float* delta;           // fp32 [H, T] workspace
-  const void* units;      // device WorkUnit[n_units], key tiles
+  const void* units;      // device WorkUnit[n_units], key tiles (8 per-die lists)
   int n_units;
-  const void* qunits;     // device WorkUnit[n_qunits], query tiles
+  const void* qunits;     // device WorkUnit[n_qunits], query tiles (8 per-die lists)
   int n_qunits;
   int rows_end;           // cu_seqlens[n]: rows past it are not touched
   int n_heads;

@@ -91,42 +91,82 @@ int check_tensor(const void* p, const char* name) {
   return DCP_OK;
 }
 
-// Tiles of `tile` rows per sequence, never straddling two sequences, in
-// longest-processing-time-first order (work of a tile: the keys it visits
-// in the forward, or the queries it visits in the backward).
-std::vector<WorkUnit> build_units(const dcp_attn_desc* d, int tile, bool keys_major) {
-  std::vector<WorkUnit> units;
-  std::vector<int64_t> work;
-  const int32_t* cu = d->cu_seqlens_host;
-  for (int32_t b = 0; b < d->n_seqs; ++b) {
-    const int32_t s0 = cu[b], len = cu[b + 1] - cu[b];
-    for (int32_t t0 = 0; t0 < len; t0 += tile) {
-      const int32_t rows = std::min(tile, len - t0);
-      units.push_back(WorkUnit{s0 + t0, rows, s0, len});
-      int64_t w;
-      if (!d->causal) {
-        w = len;
-      } else if (!keys_major) {
-        w = int64_t(t0) + rows;  // query tile sees keys [0, t0 + rows)
-      } else {
-        w = int64_t(len) - t0;  // key tile is seen by queries [t0, len)
-      }
-      work.push_back(w);
-    }
-  }
-  std::vector<size_t> idx(units.size());
-  for (size_t i = 0; i < idx.size(); ++i) idx[i] = i;
-  std::stable_sort(idx.begin(), idx.end(), [&](size_t a, size_t b) { return work[a] > work[b]; });
-  std::vector<WorkUnit> sorted(units.size());
-  for (size_t i = 0; i < idx.size(); ++i) sorted[i] = units[idx[i]];
-  return sorted;
-}
-
-size_t count_units(const dcp_attn_desc* d, int tile) {
+// Tiles of `tile` rows per (sequence, head), never straddling two
+// sequences, laid out as 8 per-die lists (see unit_for_block).  Work of a
+// tile: the keys it visits (forward, dQ pass) or the queries visiting it
+// (dK/dV pass).  The (sequence, head) groups -- split into chunks when a
+// few long sequences would otherwise leave dies idle -- are assigned to the
+// least-loaded die, longest first; each die's list keeps a chunk's tiles
+// together (they share K/V or Q/dO in that die's L2) and is padded with
+// empty tiles to the longest list.
+size_t tiles_per_head(const dcp_attn_desc* d, int tile) {
   size_t n = 0;
   for (int32_t b = 0; b < d->n_seqs; ++b)
     n += size_t((d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b] + tile - 1) / tile);
   return n;
+}
+
+std::vector<WorkUnit> build_units(const dcp_attn_desc* d, int tile, bool keys_major) {
+  const int32_t* cu = d->cu_seqlens_host;
+  const size_t total = tiles_per_head(d, tile) * size_t(d->n_heads);
+  std::vector<WorkUnit> out;
+  if (total == 0) return out;
+  const size_t cap = std::max<size_t>(4, (total + 8 * kNumXcd - 1) / (8 * kNumXcd));
+  struct Chunk {
+    int32_t b, h, t_begin, t_end;
+    int64_t work;
+  };
+  std::vector<Chunk> chunks;
+  auto tile_work = [&](int32_t len, int32_t t0, int32_t rows) -> int64_t {
+    if (!d->causal) return len;
+    return keys_major ? int64_t(len) - t0 : int64_t(t0) + rows;
+  };
+  for (int32_t b = 0; b < d->n_seqs; ++b) {
+    const int32_t len = cu[b + 1] - cu[b];
+    const int32_t nt = (len + tile - 1) / tile;
+    for (int32_t h = 0; h < d->n_heads; ++h)
+      for (int32_t c0 = 0; c0 < nt; c0 += int32_t(cap)) {
+        Chunk c{b, h, c0, std::min<int32_t>(nt, c0 + int32_t(cap)), 0};
+        for (int32_t t = c.t_begin; t < c.t_end; ++t)
+          c.work += tile_work(len, t * tile, std::min(tile, len - t * tile));
+        chunks.push_back(c);
+      }
+  }
+  std::stable_sort(chunks.begin(), chunks.end(), [](const Chunk& x, const Chunk& y) { return x.work > y.work; });
+  std::vector<std::vector<WorkUnit>> lists(kNumXcd);
+  int64_t load[kNumXcd] = {0};
+  for (const Chunk& c : chunks) {
+    int x = 0;
+    for (int i = 1; i < kNumXcd; ++i)
+      if (load[i] < load[x]) x = i;
+    load[x] += c.work;
+    const int32_t s0 = cu[c.b], len = cu[c.b + 1] - cu[c.b];
+    // within a chunk, the tile with the most work first (causal: the last
+    // query tiles of the forward, the first key tiles of the dK/dV pass)
+    const bool reverse = d->causal && !keys_major;
+    for (int32_t i = c.t_begin; i < c.t_end; ++i) {
+      const int32_t t = reverse ? c.t_end - 1 - (i - c.t_begin) : i;
+      WorkUnit u{};
+      u.row0 = s0 + t * tile;
+      u.rows = std::min(tile, len - t * tile);
+      u.seq0 = s0;
+      u.seqlen = len;
+      u.head = c.h;
+      lists[size_t(x)].push_back(u);
+    }
+  }
+  size_t per = 0;
+  for (const auto& l : lists) per = std::max(per, l.size());
+  out.assign(per * kNumXcd, WorkUnit{});
+  for (int x = 0; x < kNumXcd; ++x)
+    std::copy(lists[size_t(x)].begin(), lists[size_t(x)].end(), out.begin() + ptrdiff_t(size_t(x) * per));
+  return out;
+}
+
+// Upper bound on build_units' length (padding included) for workspace
+// sizing: no die list is longer than the total tile count.
+size_t count_units(const dcp_attn_desc* d, int tile) {
+  return tiles_per_head(d, tile) * size_t(d->n_heads) * kNumXcd;
 }
 
 struct BwdLayout {
@@ -146,6 +186,23 @@ int upload_units(const std::vector<WorkUnit>& units, void* dst, hipStream_t stre
   hipError_t e = hipMemcpyAsync(dst, units.data(), units.size() * sizeof(WorkUnit), hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
   return DCP_OK;
+}
+
+// The constant block at the head of a workspace, followed by a work list,
+// uploaded with one copy: 16-byte chunks the kernels' direct-to-LDS copies
+// read for pad columns ([0 x 8] and [1, 0 x 7] in bf16).
+int upload_consts_and_units(const std::vector<WorkUnit>& units, void* dst, hipStream_t stream) {
+  std::vector<unsigned char> buf(kConstBytes + units.size() * sizeof(WorkUnit), 0);
+  const uint16_t one = 0x3F80;  // bf16 1.0
+  std::memcpy(buf.data() + kConstOnes * 2, &one, sizeof one);
+  if (!units.empty()) std::memcpy(buf.data() + kConstBytes, units.data(), units.size() * sizeof(WorkUnit));
+  hipError_t e = hipMemcpyAsync(dst, buf.data(), buf.size(), hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
+  return DCP_OK;
+}
+
+size_t fwd_workspace_bytes(const dcp_attn_desc* d) {
+  return align_up(kConstBytes + sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, fwd_tile_rows(d->head_dim))));
 }
 
 }  // namespace
@@ -170,7 +227,7 @@ extern "C" int dcp_varlen_attn_fwd_workspace_size(const dcp_attn_desc* desc, siz
   int st = validate_desc(desc);
   if (st) return st;
   if (!bytes) return fail(DCP_ERR_INVALID, "bytes is null");
-  *bytes = align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(desc, fwd_tile_rows(desc->head_dim))));
+  *bytes = fwd_workspace_bytes(desc);
   return DCP_OK;
 }
 
@@ -193,7 +250,7 @@ extern "C" int dcp_varlen_attn_fwd(const dcp_attn_desc* desc, const void* q, con
     return st;
   if (!lse || reinterpret_cast<uintptr_t>(lse) % 4) return fail(DCP_ERR_INVALID, "lse is null or misaligned");
   const int tile = fwd_tile_rows(desc->head_dim);
-  const size_t need = align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(desc, tile)));
+  const size_t need = fwd_workspace_bytes(desc);
   if (!workspace || workspace_bytes < need)
     return fail(DCP_ERR_WORKSPACE, "forward workspace needs %zu bytes, got %zu", need, workspace_bytes);
   if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(DCP_ERR_INVALID, "workspace must be 16-byte aligned");
@@ -201,8 +258,9 @@ extern "C" int dcp_varlen_attn_fwd(const dcp_attn_desc* desc, const void* q, con
   const std::vector<WorkUnit> units = build_units(desc, tile, false);
   if (units.empty()) return DCP_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = upload_units(units, workspace, s))) return st;
-  FwdArgs a{q, k, v, o, lse, workspace, int(units.size()), desc->n_heads, desc->head_dim,
+  if ((st = upload_consts_and_units(units, workspace, s))) return st;
+  char* ws = static_cast<char*>(workspace);
+  FwdArgs a{q, k, v, o, lse, ws, ws + kConstBytes, int(units.size()), desc->n_heads, desc->head_dim,
             int(desc->total_tokens), desc->scale, desc->causal, s};
   hipError_t e = launch_fwd(a);
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "forward launch: %s", hipGetErrorString(e));
@@ -274,7 +332,7 @@ ProfLayout prof_layout(int64_t max_len, const dcp_profile_opts* o) {
   l.lse = align_up(size_t(max_len) * size_t(o->n_heads) * 4);
   int32_t cu[2] = {0, int32_t(max_len)};
   dcp_attn_desc d{1, cu, max_len, o->n_heads, o->head_dim, 1.f, o->causal};
-  const size_t fw = align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(&d, fwd_tile_rows(o->head_dim))));
+  const size_t fw = fwd_workspace_bytes(&d);
   l.ws_bytes = std::max(fw, bwd_layout(&d).total);
   l.ws_off = 8 * l.tensor + l.lse;
   l.total = l.ws_off + l.ws_bytes;
