@@ -3,12 +3,14 @@
 // packed sequences of Sec. 1).
 //
 // Three launches, no atomics, bitwise deterministic:
-//   1. bwd_delta:  Delta = rowsum(dO o O) per (row, head), fp32.
-//   2. bwd_dkdv:   key-stationary.  One workgroup per (key tile of 32*NW
-//                  rows, head); each wavefront keeps 32 keys' K and V
-//                  fragments and their dK, dV accumulators in registers and
-//                  walks the query tiles of its own sequence (on or below the
-//                  diagonal when causal), Q / dO tiles double-buffered in LDS:
+//   1. bwd_delta:  -Delta = -rowsum(dO o O) and LSE*log2e per (row, head),
+//                  fp32.
+//   2. bwd_dkdv:   key-stationary.  One workgroup per (key tile, head);
+//                  each wavefront keeps the K and V fragments of 32 or 64
+//                  keys and their dK, dV accumulators in registers and walks
+//                  the query tiles of its own sequence (on or below the
+//                  diagonal when causal), Q / dO tiles streaming through an
+//                  LDS ring:
 //                    S  = Q K^T,  dP = dO V^T         (A from LDS, B in regs)
 //                    P  = exp2(S*scale*log2e - LSE*log2e)
 //                    dS = P o (dP - Delta)
@@ -50,11 +52,13 @@ struct BwdShape {
 };
 
 // ---------------------------------------------------------------------------
-// 1. Delta = rowsum(dO o O); 16 lanes per (row, head), lane c covers 8c..8c+7.
+// 1. -Delta = -rowsum(dO o O) and LSE*log2e per (row, head), fp32 [H, T];
+// 16 lanes per (row, head), lane c covers columns 8c..8c+7.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict__ dout,
-                                                        const __bf16* __restrict__ o, float* __restrict__ delta,
-                                                        int rows_end, int H, int T) {
+                                                        const __bf16* __restrict__ o,
+                                                        const float* __restrict__ lse, float* __restrict__ ndelta,
+                                                        float* __restrict__ lse2, int rows_end, int H, int T) {
   constexpr int CPR = D / 8;
   const int64_t pair = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) >> 4;
   const int c = threadIdx.x & 15;
@@ -74,7 +78,8 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict
   if (pair < n_pairs && c == 0) {
     const int64_t row = pair / H;
     const int hh = int(pair % H);
-    delta[int64_t(hh) * T + row] = part;
+    ndelta[int64_t(hh) * T + row] = -part;
+    lse2[int64_t(hh) * T + row] = lse[int64_t(hh) * T + row] * kLog2e;
   }
 }
 
@@ -114,291 +119,320 @@ __device__ __forceinline__ void store_rows_bf16(const f32x16 (&acc)[NDB], float 
 
 // ---------------------------------------------------------------------------
 // 2. dK, dV (key-stationary).
-template <int D, int NW, bool CAUSAL>
+//
+// Each wavefront owns 32*KB keys: their K and V fragments (B operands of
+// S = Q K^T and dP = dO V^T) and their dK, dV accumulators stay in
+// registers for the whole query loop.  Query tiles of BM rows stream
+// through an NSTAGE-deep LDS ring filled by direct global-to-LDS copies
+// NSTAGE - 1 tiles ahead, one barrier per tile: Q and dO twice each (rows
+// read 16 B per lane for the A operands of S and dP, rows read by
+// transposing reads for the B operands of dV and dK, each copy at its
+// conflict-free stride), plus LSE*log2e and -Delta of the tile's queries.
+// -Delta is the initial value of the dP accumulator, so the products yield
+// dP - Delta directly.  With KB = 2 every operand fetched from LDS feeds
+// two matrix products, and the exponentials of one key block can overlap
+// the products of the other.
+template <int D, int KB, int NW, int NSTAGE, bool CAUSAL>
 __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
-    const __bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
-    __bf16* __restrict__ dk, __bf16* __restrict__ dv, const WorkUnit* __restrict__ units, int per_xcd, int H, int T, float scale,
-    float scale_log2) {
+    const __bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
+    __bf16* __restrict__ dk, __bf16* __restrict__ dv, const __bf16* __restrict__ consts,
+    const WorkUnit* __restrict__ units, int per_xcd, int H, int T, float scale, float scale_log2) {
   using S = BwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
-  // Q and dO are each kept twice per buffer: rows read 16 B per lane (A
-  // operands of S and dP) and rows read by transposing reads (B operands of
-  // dK and dV), each with its conflict-free stride.
-  constexpr int RSTR = S::DP + 8;
+  constexpr int RSTR = S::DP + 8;  // an odd number of 16-byte chunks
   constexpr int TSTR = S::TSTR;
-  constexpr int NT = 64 * NW;
-  constexpr int BM = kBwdBM;  // queries per step
-  constexpr int NCHQ = BM * CPR;
-  constexpr int CPTQ = (NCHQ + NT - 1) / NT;
+  constexpr int BM = kBwdBM;  // queries per tile
+  using DR = DmaTile<BM, RSTR / 8, CPR, NW>;
+  using DT = DmaTile<BM, TSTR / 8, CPR, NW>;
+  using DL = DmaVec<BM, NW>;
+  constexpr int NI = 2 * DR::NI + 2 * DT::NI + 2 * DL::NI;  // copies per wavefront per tile
   constexpr int RBUF = BM * RSTR, TBUF = BM * TSTR;
-  constexpr int SLOT = 2 * RBUF + 2 * TBUF;  // one double-buffered tensor
-  constexpr int SSTR = S::RSTR;              // epilogue staging stride
-
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * SLOT];
-  __bf16* const Qr = lds;                    // [2][BM][RSTR]
-  __bf16* const Qt = lds + 2 * RBUF;         // [2][BM][TSTR]
-  __bf16* const dOr = lds + SLOT;
-  __bf16* const dOt = lds + SLOT + 2 * RBUF;
-  __shared__ __attribute__((aligned(16))) float lse_s[2 * BM];
-  __shared__ __attribute__((aligned(16))) float dlt_s[2 * BM];
-  static_assert(2 * SLOT >= NW * 32 * SSTR, "staging area too small");
+  constexpr int SSTR = S::RSTR;  // epilogue staging stride
+  __shared__ __attribute__((aligned(16))) __bf16 Qr[NSTAGE * RBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 dOr[NSTAGE * RBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 Qt[NSTAGE * TBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 dOt[NSTAGE * TBUF];
+  __shared__ __attribute__((aligned(16))) float LV[NSTAGE * 2 * BM];  // LSE*log2e | -Delta
+  constexpr int NSB = NW * KB;  // 32-key blocks per workgroup
+  static_assert(NSB % 2 == 0 && NSTAGE * RBUF >= NSB / 2 * 32 * SSTR, "staging area too small");
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "ring depth");
 
   const WorkUnit u = unit_for_block(units, per_xcd);
   if (u.rows == 0) return;
   const int h = u.head;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches on it
   const int g = lane >> 5;
   const int j = lane & 31;
   const int64_t ts = int64_t(H) * D;
   const int seqlen = u.seqlen;
   const int key_t0 = u.row0 - u.seq0;  // first key of the workgroup, sequence-relative
+  const __bf16* zero = consts + kConstZero;
+  const float* fzero = reinterpret_cast<const float*>(consts + kConstZero);
+  const float* finf = reinterpret_cast<const float*>(consts + kConstInf);
 
   const __bf16* qh = q + int64_t(u.seq0) * ts + int64_t(h) * D;
   const __bf16* kh = k + int64_t(u.seq0) * ts + int64_t(h) * D;
   const __bf16* vh = v + int64_t(u.seq0) * ts + int64_t(h) * D;
   const __bf16* doh = dout + int64_t(u.seq0) * ts + int64_t(h) * D;
-  const float* lseh = lse + int64_t(h) * T + u.seq0;
-  const float* dlth = delta + int64_t(h) * T + u.seq0;
+  const float* lseh = lse2 + int64_t(h) * T + u.seq0;
+  const float* ndh = ndelta + int64_t(h) * T + u.seq0;
 
-  // Pad columns are never written by tile loads; the contraction reads
-  // columns up to DP and the transposing reads up to NDB*32.
-  for (int i = tid; i < 2 * BM * (RSTR - D); i += NT) {
-    const int r = i / (RSTR - D), c = D + i % (RSTR - D);
-    Qr[r * RSTR + c] = __bf16(0.f);
-    dOr[r * RSTR + c] = __bf16(0.f);
-  }
-  for (int i = tid; i < 2 * BM * (TSTR - D); i += NT) {
-    const int r = i / (TSTR - D), c = D + i % (TSTR - D);
-    Qt[r * TSTR + c] = __bf16(0.f);
-    dOt[r * TSTR + c] = __bf16(0.f);
-  }
-
-  // K and V fragments (B operands of S = Q K^T and dP = dO V^T): lane (g, j)
-  // holds key j of this wavefront, columns 16*kd + 8*g .. +7.  Keys past the
-  // sequence end are zero; their dK, dV rows are never stored.
-  const int my_key = 32 * wave + j;  // tile-relative
-  const bool key_ok = my_key < u.rows;
-  bf16x8 kf[NKD], vf[NKD];
+  // K and V fragments: lane (g, j) of key block kb holds key 32*(KB*wave +
+  // kb) + j of the tile, columns 16*kd + 8*g .. +7.  Keys past the sequence
+  // end are zero; their dK, dV rows are never stored.
+  bf16x8 kf[KB][NKD], vf[KB][NKD];
 #pragma unroll
-  for (int kd = 0; kd < NKD; ++kd) {
-    const int col = 16 * kd + 8 * g;
-    if (key_ok && col < D) {
-      kf[kd] = *reinterpret_cast<const bf16x8*>(kh + int64_t(key_t0 + my_key) * ts + col);
-      vf[kd] = *reinterpret_cast<const bf16x8*>(vh + int64_t(key_t0 + my_key) * ts + col);
-    } else {
-      kf[kd] = bf16x8{};
-      vf[kd] = bf16x8{};
-    }
-  }
-
-  const int q_begin = CAUSAL ? (key_t0 / BM) * BM : 0;
-  const int n_qt = (seqlen - q_begin + BM - 1) / BM;
-  const int key_seq = key_t0 + my_key;
-
-  u32x4 qreg[CPTQ], doreg[CPTQ];
-  float lse_reg = INFINITY, dlt_reg = 0.f;
-  auto load_q_tile = [&](int q0) {
-#pragma unroll
-    for (int c = 0; c < CPTQ; ++c) {
-      const int ch = tid + NT * c;
-      if (NCHQ % NT == 0 || ch < NCHQ) {
-        const int r = ch / CPR, cc = ch % CPR;
-        if (q0 + r < seqlen) {
-          qreg[c] = *reinterpret_cast<const u32x4*>(qh + int64_t(q0 + r) * ts + cc * 8);
-          doreg[c] = *reinterpret_cast<const u32x4*>(doh + int64_t(q0 + r) * ts + cc * 8);
-        } else {
-          qreg[c] = u32x4{0, 0, 0, 0};
-          doreg[c] = u32x4{0, 0, 0, 0};
-        }
-      }
-    }
-    if (tid < BM) {
-      // A query past the sequence end gets LSE = +inf, so its P is exactly 0.
-      const bool ok = q0 + tid < seqlen;
-      lse_reg = ok ? lseh[q0 + tid] * kLog2e : INFINITY;
-      dlt_reg = ok ? dlth[q0 + tid] : 0.f;
-    }
-  };
-  auto store_q_tile = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < CPTQ; ++c) {
-      const int ch = tid + NT * c;
-      if (NCHQ % NT == 0 || ch < NCHQ) {
-        const int r = ch / CPR, cc = ch % CPR;
-        *reinterpret_cast<u32x4*>(&Qr[buf * RBUF + r * RSTR + cc * 8]) = qreg[c];
-        *reinterpret_cast<u32x4*>(&Qt[buf * TBUF + r * TSTR + cc * 8]) = qreg[c];
-        *reinterpret_cast<u32x4*>(&dOr[buf * RBUF + r * RSTR + cc * 8]) = doreg[c];
-        *reinterpret_cast<u32x4*>(&dOt[buf * TBUF + r * TSTR + cc * 8]) = doreg[c];
-      }
-    }
-    if (tid < BM) {
-      lse_s[buf * BM + tid] = lse_reg;
-      dlt_s[buf * BM + tid] = dlt_reg;
-    }
-  };
-
-  f32x16 dk_acc[NDB], dv_acc[NDB];
-#pragma unroll
-  for (int db = 0; db < NDB; ++db) {
-    dk_acc[db] = f32x16{};
-    dv_acc[db] = f32x16{};
-  }
-
-  if (n_qt > 0) {
-    load_q_tile(q_begin);
-    store_q_tile(0);
-  }
-  __syncthreads();
-
-  const int tr_row = (lane & 15) >> 2;
-  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  const int wave_key_lo = key_t0 + 32 * wave;  // smallest key of this wavefront
-
-  // One 32-query block against this wavefront's 32 keys.  MASK applies the
-  // causal mask (only blocks crossing the diagonal need it).
-  auto process_block = [&](int buf, int q0, int qb, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    const __bf16* Qb = &Qr[buf * RBUF];
-    const __bf16* dOb = &dOr[buf * RBUF];
-    const __bf16* Qtb = &Qt[buf * TBUF];
-    const __bf16* dOtb = &dOt[buf * TBUF];
-    const float* lseb = &lse_s[buf * BM];
-    const float* dltb = &dlt_s[buf * BM];
-    f32x16 s = f32x16{}, dp = f32x16{};
+  for (int kb = 0; kb < KB; ++kb) {
+    const int key = 32 * (KB * wave + kb) + j;
+    const bool ok = key < u.rows;
 #pragma unroll
     for (int kd = 0; kd < NKD; ++kd) {
-      const bf16x8 aq = lds_read_b128(&Qb[(32 * qb + j) * RSTR + 16 * kd + 8 * g]);
-      s = mfma32(aq, kf[kd], s);
-      const bf16x8 ado = lds_read_b128(&dOb[(32 * qb + j) * RSTR + 16 * kd + 8 * g]);
-      dp = mfma32(ado, vf[kd], dp);
-    }
-    // This lane holds key `key_seq` against queries 32qb + 8b + 4g + c.
-    bf16x8 pa[2], da[2];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lseb[32 * qb + 8 * b + 4 * g]);
-      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dltb[32 * qb + 8 * b + 4 * g]);
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int r = 4 * b + c;
-        float p = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -l4[c]));
-        if (MASK && key_seq > q0 + 32 * qb + 8 * b + 4 * g + c) p = 0.f;
-        pa[b >> 1][4 * (b & 1) + c] = __bf16(p);
-        da[b >> 1][4 * (b & 1) + c] = __bf16(p * (dp[r] - d4[c]));
+      const int col = 16 * kd + 8 * g;
+      if (ok && col < D) {
+        kf[kb][kd] = *reinterpret_cast<const bf16x8*>(kh + int64_t(key_t0 + key) * ts + col);
+        vf[kb][kd] = *reinterpret_cast<const bf16x8*>(vh + int64_t(key_t0 + key) * ts + col);
+      } else {
+        kf[kb][kd] = bf16x8{};
+        vf[kb][kd] = bf16x8{};
       }
     }
-    // dV += P^T dO and dK += dS^T Q: B = rows (queries) x columns (d),
-    // fetched column-wise with transposing reads.
+  }
+  wait_vmcnt<0>();  // settle the fragment loads before the first copy
+
+  const int wave_key_lo = key_t0 + 32 * KB * wave;  // smallest key of this wavefront
+  const int q_begin = CAUSAL ? (key_t0 / BM) * BM : 0;
+  const int n_qt = (seqlen - q_begin + BM - 1) / BM;
+
+  auto issue_tile = [&](int it) {
+    const unsigned st = unsigned(it) % NSTAGE;
+    const int q0 = q_begin + it * BM;
+    const int valid = seqlen - q0;
+    const __bf16* qs = qh + int64_t(q0) * ts;
+    const __bf16* ds = doh + int64_t(q0) * ts;
+    DR::issue(&Qr[st * RBUF], qs, ts, valid, zero, zero, wave, lane);
+    DT::issue(&Qt[st * TBUF], qs, ts, valid, zero, zero, wave, lane);
+    DR::issue(&dOr[st * RBUF], ds, ts, valid, zero, zero, wave, lane);
+    DT::issue(&dOt[st * TBUF], ds, ts, valid, zero, zero, wave, lane);
+    // A query past the sequence end gets LSE = +inf, so its P is exactly 0.
+    DL::issue(&LV[st * 2 * BM], lseh + q0, valid, finf, wave, lane);
+    DL::issue(&LV[st * 2 * BM + BM], ndh + q0, valid, fzero, wave, lane);
+  };
+  // Waits until tile it+1 has landed (tile it+2 may stay in flight).
+  auto wait_next = [&](int it) {
+    if (NSTAGE == 3 && it + 2 < n_qt)
+      wait_vmcnt<NI>();
+    else
+      wait_vmcnt<0>();
+  };
+
+  f32x16 dk_acc[KB][NDB], dv_acc[KB][NDB];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
+      dk_acc[kb][db] = f32x16{};
+      dv_acc[kb][db] = f32x16{};
+    }
+
+  issue_tile(0);
+  if (NSTAGE == 3 && n_qt > 1) issue_tile(1);
+  wait_next(-1);
+  __syncthreads();
+
+  // This lane's element offsets inside a tile: 16-byte row reads (A
+  // operands) and transposing reads (see lds_read_tr); every other term is
+  // a compile-time constant.
+  const unsigned ar_off = j * RSTR + 8 * g;
+  const unsigned tr_off = (4 * g + ((lane & 15) >> 2)) * TSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const lds_bf16* Qr3 = lds_ptr(Qr);
+  const lds_bf16* dOr3 = lds_ptr(dOr);
+  const lds_bf16* Qt3 = lds_ptr(Qt);
+  const lds_bf16* dOt3 = lds_ptr(dOt);
+  const lds_f32* LV3 = lds_ptr(LV);
+
+  // One 32-query block (first query qa, sequence-relative) of stage st
+  // against this wavefront's 32*KB keys.  MASK applies the causal mask.
+  auto process_block = [&](unsigned st, int qb, int qa, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    unsigned rb = st * RBUF + 32 * qb * RSTR + ar_off;
+    unsigned tb = st * TBUF + 32 * qb * TSTR + tr_off;
+    unsigned lb = st * 2 * BM + 32 * qb + 4 * g;
+    // Opaque to the optimizer: each read below is then one of these bases
+    // plus a constant, which folds into the instruction's offset field
+    // (otherwise every read's address is rebuilt with vector arithmetic).
+    asm("" : "+v"(rb), "+v"(tb), "+v"(lb));
+    bf16x8 aq[NKD], ado[NKD];
+#pragma unroll
+    for (int kd = 0; kd < NKD; ++kd) {
+      aq[kd] = lds_read_b128(Qr3 + rb + 16 * kd);
+      ado[kd] = lds_read_b128(dOr3 + rb + 16 * kd);
+    }
+    // Lane (g, j) of an S / dP accumulator holds key j of its key block
+    // against queries qa + 8b + 4g + c (register 4b + c).
+    f32x16 nd;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const f32x4 t = lds_read_f32x4(LV3 + lb + BM + 8 * b);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) nd[4 * b + c] = t[c];
+    }
+    f32x16 s[KB], dp[KB];
+    mfma_prio_hi();
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      s[kb] = f32x16{};
+#pragma unroll
+      for (int kd = 0; kd < NKD; ++kd) s[kb] = mfma32(aq[kd], kf[kb][kd], s[kb]);
+      dp[kb] = nd;
+#pragma unroll
+      for (int kd = 0; kd < NKD; ++kd) dp[kb] = mfma32(ado[kd], vf[kb][kd], dp[kb]);
+    }
+    mfma_prio_lo();
+    f32x4 l4[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) l4[b] = lds_read_f32x4(LV3 + lb + 8 * b);
+    bf16x8 pa[KB][2], da[KB][2];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const int key = wave_key_lo + 32 * kb + j;
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int r = 4 * b + c;
+          float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], scale_log2, -l4[b][c]));
+          if (MASK && key > qa + 8 * b + 4 * g + c) p = 0.f;
+          pa[kb][b >> 1][4 * (b & 1) + c] = __bf16(p);
+          da[kb][b >> 1][4 * (b & 1) + c] = __bf16(p * dp[kb][r]);
+        }
+    }
+    // dV += P^T dO and dK += dS^T Q: B = rows (queries) x columns (d),
+    // fetched column-wise with transposing reads, shared by the key blocks.
+    bf16x8 bdo[NDB][2], bq[NDB][2];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        const int off = (32 * qb + 16 * hh + 4 * g + tr_row) * TSTR + 32 * db + tr_col;
-        const bf16x8 bdo = cat(lds_read_tr(&dOtb[off]), lds_read_tr(&dOtb[off + 8 * TSTR]));
-        dv_acc[db] = mfma32(pa[hh], bdo, dv_acc[db]);
-        const bf16x8 bq = cat(lds_read_tr(&Qtb[off]), lds_read_tr(&Qtb[off + 8 * TSTR]));
-        dk_acc[db] = mfma32(da[hh], bq, dk_acc[db]);
+        const unsigned o = tb + 16 * hh * TSTR + 32 * db;
+        bdo[db][hh] = cat(lds_read_tr(dOt3 + o), lds_read_tr(dOt3 + o + 8 * TSTR));
+        bq[db][hh] = cat(lds_read_tr(Qt3 + o), lds_read_tr(Qt3 + o + 8 * TSTR));
       }
-    }
+    mfma_prio_hi();
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          dv_acc[kb][db] = mfma32(pa[kb][hh], bdo[db][hh], dv_acc[kb][db]);
+          dk_acc[kb][db] = mfma32(da[kb][hh], bq[db][hh], dk_acc[kb][db]);
+        }
+    mfma_prio_lo();
   };
 
   // Query tiles are walked in two phases per wavefront: (causal only) those
-  // crossing its diagonal, where blocks entirely above its keys are skipped
-  // and the rest masked, then those needing no mask.  Both phases run the
-  // same load / store / barrier sequence.
+  // reaching its keys, where 32-query blocks entirely before its keys are
+  // skipped and blocks crossing them masked, then those needing no mask.
+  // Every iteration runs the same copy / wait / barrier sequence.
   auto run = [&](int it0, int it1, auto mask_tag) {
     constexpr bool MASK = decltype(mask_tag)::value;
     for (int it = it0; it < it1; ++it) {
-      const int buf = it & 1;
+      if (it + NSTAGE - 1 < n_qt) issue_tile(it + NSTAGE - 1);
+      const unsigned st = unsigned(it) % NSTAGE;
       const int q0 = q_begin + it * BM;
-      if (it + 1 < n_qt) load_q_tile(q0 + BM);
 #pragma unroll
       for (int qb = 0; qb < BM / 32; ++qb) {
+        const int qa = q0 + 32 * qb;
+        if (qa >= seqlen) continue;  // padding rows of the last tile
         if (MASK) {
-          const int qa = q0 + 32 * qb;
           if (qa + 31 < wave_key_lo) continue;  // every query precedes every key
-          if (qa >= wave_key_lo + 31) {
-            process_block(buf, q0, qb, std::false_type{});
+          if (qa >= wave_key_lo + 32 * KB - 1) {
+            process_block(st, qb, qa, std::false_type{});
             continue;
           }
         }
-        process_block(buf, q0, qb, std::integral_constant<bool, MASK>{});
+        process_block(st, qb, qa, std::integral_constant<bool, MASK>{});
       }
-      if (it + 1 < n_qt) store_q_tile(buf ^ 1);
+      wait_next(it);
       __syncthreads();
     }
   };
   int it_plain = 0;
   if (CAUSAL) {
-    // first step whose queries all follow all of this wavefront's keys
-    it_plain = min(n_qt, max(0, (wave_key_lo + 31 - q_begin + BM - 1) / BM));
+    // first tile whose queries all follow all of this wavefront's keys
+    it_plain = min(n_qt, max(0, (wave_key_lo + 32 * KB - 1 - q_begin + BM - 1) / BM));
     run(0, it_plain, std::true_type{});
   }
   run(it_plain, n_qt, std::false_type{});
 
-  // Epilogue through LDS (the tile buffers are free now): each wavefront
-  // stages its 32 rows of dK, then of dV.
-  __bf16* stage = lds + wave * 32 * SSTR;  // 32 rows per wavefront
-  const int n_rows = max(0, min(32, u.rows - 32 * wave));
-  __bf16* dk_base = dk + int64_t(u.row0 + 32 * wave) * ts + int64_t(h) * D;
-  __bf16* dv_base = dv + int64_t(u.row0 + 32 * wave) * ts + int64_t(h) * D;
-  store_rows_bf16<D, NDB>(dk_acc, scale, stage, SSTR, dk_base, ts, n_rows, lane);
-  store_rows_bf16<D, NDB>(dv_acc, 1.f, stage, SSTR, dv_base, ts, n_rows, lane);
+  // Epilogue through LDS (the ring is idle now): the workgroup's first half
+  // of 32-key blocks is staged in the Q buffers, the second in the dO
+  // buffers, dK first, then dV.
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) {
+    const int sb = KB * wave + kb;
+    const int key0 = 32 * sb;
+    __bf16* stage = sb < NSB / 2 ? Qr + sb * 32 * SSTR : dOr + (sb - NSB / 2) * 32 * SSTR;
+    const int n_rows = max(0, min(32, u.rows - key0));
+    __bf16* dk_base = dk + int64_t(u.row0 + key0) * ts + int64_t(h) * D;
+    __bf16* dv_base = dv + int64_t(u.row0 + key0) * ts + int64_t(h) * D;
+    store_rows_bf16<D, NDB>(dk_acc[kb], scale, stage, SSTR, dk_base, ts, n_rows, lane);
+    store_rows_bf16<D, NDB>(dv_acc[kb], 1.f, stage, SSTR, dv_base, ts, n_rows, lane);
+  }
 }
 
 // ---------------------------------------------------------------------------
 // 3. dQ (query-stationary).
-template <int D, int NW, bool CAUSAL>
+//
+// Each wavefront keeps 32 queries' Q and dO fragments (B operands), their
+// LSE*log2e and -Delta in registers while key tiles of BN rows stream
+// through an NSTAGE-deep LDS ring filled by direct global-to-LDS copies
+// NSTAGE - 1 tiles ahead (K twice: rows read 16 B per lane for S^T, rows
+// read by transposing reads for dQ^T; V once), one barrier per tile.
+template <int D, int NW, int NSTAGE, bool CAUSAL>
 __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
-    const __bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
-    __bf16* __restrict__ dq, const WorkUnit* __restrict__ units, int per_xcd, int H, int T, float scale, float scale_log2) {
+    const __bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
+    __bf16* __restrict__ dq, const __bf16* __restrict__ consts, const WorkUnit* __restrict__ units, int per_xcd,
+    int H, int T, float scale, float scale_log2) {
   using S = BwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
   constexpr int KSTR = S::DP + 8;  // K and V rows read 16 B per lane
   constexpr int TSTR = S::TSTR;    // second copy of K for transposing reads
   constexpr int BN = kBwdDqBN;
-  constexpr int NT = 64 * NW;
-  constexpr int NCH = BN * CPR;
-  constexpr int CPT = (NCH + NT - 1) / NT;
   constexpr int KBUF = BN * KSTR, TBUF = BN * TSTR;
+  using DK = DmaTile<BN, KSTR / 8, CPR, NW>;
+  using DT = DmaTile<BN, TSTR / 8, CPR, NW>;
+  constexpr int NI = 2 * DK::NI + DT::NI;  // copies per wavefront per tile
 
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[2 * KBUF];
-  __shared__ __attribute__((aligned(16))) __bf16 Vs[2 * KBUF];
-  __shared__ __attribute__((aligned(16))) __bf16 Kt[2 * TBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[NSTAGE * KBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[NSTAGE * KBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 Kt[NSTAGE * TBUF];
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "ring depth");
 
   const WorkUnit u = unit_for_block(units, per_xcd);
   if (u.rows == 0) return;
   const int h = u.head;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches on it
   const int g = lane >> 5;
   const int j = lane & 31;
   const int64_t ts = int64_t(H) * D;
   const int seqlen = u.seqlen;
   const int tile_q0 = u.row0 - u.seq0;
   const int wave_q0 = tile_q0 + 32 * wave;
+  const __bf16* zero = consts + kConstZero;
 
   const __bf16* qh = q + int64_t(u.seq0) * ts + int64_t(h) * D;
   const __bf16* kh = k + int64_t(u.seq0) * ts + int64_t(h) * D;
   const __bf16* vh = v + int64_t(u.seq0) * ts + int64_t(h) * D;
   const __bf16* doh = dout + int64_t(u.seq0) * ts + int64_t(h) * D;
 
-  for (int i = tid; i < 2 * BN * (KSTR - D); i += NT) {
-    const int r = i / (KSTR - D), c = D + i % (KSTR - D);
-    Ks[r * KSTR + c] = __bf16(0.f);
-    Vs[r * KSTR + c] = __bf16(0.f);
-  }
-  for (int i = tid; i < 2 * BN * (TSTR - D); i += NT) {
-    const int r = i / (TSTR - D), c = D + i % (TSTR - D);
-    Kt[r * TSTR + c] = __bf16(0.f);
-  }
-
-  // Per-lane query state: Q and dO fragments (B operands), LSE, Delta.
+  // Per-lane query state: Q and dO fragments (B operands), LSE, -Delta.
   const int qrel = 32 * wave + j;
   const bool q_ok = qrel < u.rows;
   const int my_q = tile_q0 + qrel;  // sequence-relative
@@ -414,107 +448,109 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
       df[kd] = bf16x8{};
     }
   }
-  const float lse2 = q_ok ? lse[int64_t(h) * T + u.seq0 + my_q] * kLog2e : INFINITY;
-  const float dlt = q_ok ? delta[int64_t(h) * T + u.seq0 + my_q] : 0.f;
+  const float lse_l2 = q_ok ? lse2[int64_t(h) * T + u.seq0 + my_q] : INFINITY;
+  const float ndlt = q_ok ? ndelta[int64_t(h) * T + u.seq0 + my_q] : 0.f;
+  // -Delta as the initial dP^T accumulator, so the products yield
+  // dP^T - Delta (at head width 128 the 16 registers it takes are not
+  // spare: there the difference is taken per element instead).
+  constexpr bool FOLD = D <= 96;
+  f32x16 nd_init;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) nd_init[r] = FOLD ? ndlt : 0.f;
+  wait_vmcnt<0>();  // settle the fragment loads before the first copy
 
   const int key_end = CAUSAL ? min(seqlen, tile_q0 + u.rows) : seqlen;
   const int n_tiles = (key_end + BN - 1) / BN;
 
-  u32x4 kreg[CPT], vreg[CPT];
-  auto load_tile = [&](int kt) {
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int ch = tid + NT * c;
-      if (NCH % NT == 0 || ch < NCH) {
-        const int r = ch / CPR, cc = ch % CPR;
-        const int key = kt * BN + r;
-        if (key < seqlen) {
-          kreg[c] = *reinterpret_cast<const u32x4*>(kh + int64_t(key) * ts + cc * 8);
-          vreg[c] = *reinterpret_cast<const u32x4*>(vh + int64_t(key) * ts + cc * 8);
-        } else {
-          kreg[c] = u32x4{0, 0, 0, 0};
-          vreg[c] = u32x4{0, 0, 0, 0};
-        }
-      }
-    }
+  auto issue_tile = [&](int kt) {
+    const unsigned st = unsigned(kt) % NSTAGE;
+    const int valid = seqlen - kt * BN;
+    const __bf16* ks = kh + int64_t(kt) * BN * ts;
+    DK::issue(&Ks[st * KBUF], ks, ts, valid, zero, zero, wave, lane);
+    DK::issue(&Vs[st * KBUF], vh + int64_t(kt) * BN * ts, ts, valid, zero, zero, wave, lane);
+    DT::issue(&Kt[st * TBUF], ks, ts, valid, zero, zero, wave, lane);
   };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int ch = tid + NT * c;
-      if (NCH % NT == 0 || ch < NCH) {
-        const int r = ch / CPR, cc = ch % CPR;
-        *reinterpret_cast<u32x4*>(&Ks[buf * KBUF + r * KSTR + cc * 8]) = kreg[c];
-        *reinterpret_cast<u32x4*>(&Vs[buf * KBUF + r * KSTR + cc * 8]) = vreg[c];
-        *reinterpret_cast<u32x4*>(&Kt[buf * TBUF + r * TSTR + cc * 8]) = kreg[c];
-      }
-    }
+  // Before the barrier that ends tile kt: tile kt+1 must have landed; only
+  // tile kt+2's copies (three stages: issued this iteration) may still be
+  // in flight.
+  auto wait_next = [&](int kt) {
+    if (NSTAGE == 3 && kt + 2 < n_tiles)
+      wait_vmcnt<NI>();
+    else
+      wait_vmcnt<0>();
   };
 
   f32x16 acc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
 
-  if (n_tiles > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
+  if (n_tiles > 0) issue_tile(0);
+  if (NSTAGE == 3 && n_tiles > 1) issue_tile(1);
+  wait_next(-1);
   __syncthreads();
 
-  const int tr_row = (lane & 15) >> 2;
-  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const unsigned ar_off = j * KSTR + 8 * g;
+  const unsigned tr_off = (4 * g + ((lane & 15) >> 2)) * TSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const lds_bf16* Ks3 = lds_ptr(Ks);
+  const lds_bf16* Vs3 = lds_ptr(Vs);
+  const lds_bf16* Kt3 = lds_ptr(Kt);
   const int wave_last_q = wave_q0 + 31;
 
   // One key tile against this wavefront's 32 queries.  MASK covers tiles
   // crossing the sequence end or the causal diagonal.
-  auto process_tile = [&](int buf, int k0, auto mask_tag) {
+  auto process_tile = [&](unsigned st, int k0, auto mask_tag) {
     constexpr bool MASK = decltype(mask_tag)::value;
-    const __bf16* Kb = &Ks[buf * KBUF];
-    const __bf16* Vb = &Vs[buf * KBUF];
-    const __bf16* Tb = &Kt[buf * TBUF];
+    unsigned rb = st * KBUF + ar_off;
+    unsigned tb = st * TBUF + tr_off;
+    asm("" : "+v"(rb), "+v"(tb));  // keeps the constant terms in the offset fields
     f32x16 s[BN / 32], dp[BN / 32];
 #pragma unroll
     for (int kb = 0; kb < BN / 32; ++kb) {
       s[kb] = f32x16{};
-      dp[kb] = f32x16{};
+      dp[kb] = FOLD ? nd_init : f32x16{};
     }
+    mfma_prio_hi();
 #pragma unroll
     for (int kd = 0; kd < NKD; ++kd) {
 #pragma unroll
       for (int kb = 0; kb < BN / 32; ++kb) {
-        const bf16x8 ak = lds_read_b128(&Kb[(32 * kb + j) * KSTR + 16 * kd + 8 * g]);
+        const bf16x8 ak = lds_read_b128(Ks3 + rb + 32 * kb * KSTR + 16 * kd);
         s[kb] = mfma32(ak, qf[kd], s[kb]);
-        const bf16x8 av = lds_read_b128(&Vb[(32 * kb + j) * KSTR + 16 * kd + 8 * g]);
+        const bf16x8 av = lds_read_b128(Vs3 + rb + 32 * kb * KSTR + 16 * kd);
         dp[kb] = mfma32(av, df[kd], dp[kb]);
       }
     }
+    mfma_prio_lo();
+    // Lane (g, j) holds query j against keys k0 + 32kb + 8(r/4) + 4g + r%4.
     bf16x8 dsb[BN / 32][2];
 #pragma unroll
     for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], scale_log2, -lse2));
+        float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], scale_log2, -lse_l2));
         if constexpr (MASK) {
           const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * g + (r & 3);
           if (key >= seqlen || (CAUSAL && key > my_q)) p = 0.f;
         }
-        dsb[kb][r >> 3][r & 7] = __bf16(p * (dp[kb][r] - dlt));
+        dsb[kb][r >> 3][r & 7] = __bf16(p * (FOLD ? dp[kb][r] : dp[kb][r] + ndlt));
       }
     // dQ^T += K^T dS^T: A = K^T (rows d, keys 32kb + 16hh + 4g + {0..3, 8..11}).
+    mfma_prio_hi();
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int kb = 0; kb < BN / 32; ++kb)
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
-          const __bf16* p = &Tb[(32 * kb + 16 * hh + 4 * g + tr_row) * TSTR + 32 * db + tr_col];
-          const bf16x8 a = cat(lds_read_tr(p), lds_read_tr(p + 8 * TSTR));
+          const unsigned o = tb + (32 * kb + 16 * hh) * TSTR + 32 * db;
+          const bf16x8 a = cat(lds_read_tr(Kt3 + o), lds_read_tr(Kt3 + o + 8 * TSTR));
           acc[db] = mfma32(a, dsb[kb][hh], acc[db]);
         }
+    mfma_prio_lo();
   };
 
   // Key tiles in up to three phases per wavefront (unmasked, masked, idle),
-  // each with the same load / store / barrier sequence.
+  // each with the same copy / wait / barrier sequence.
   int t_mask = min(n_tiles, seqlen / BN);
   int t_idle = n_tiles;
   if (CAUSAL) {
@@ -524,11 +560,11 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   auto run = [&](int kt0, int kt1, auto mode_tag) {
     constexpr int MODE = decltype(mode_tag)::value;  // 0 unmasked, 1 masked, 2 idle
     for (int kt = kt0; kt < kt1; ++kt) {
-      const int buf = kt & 1;
-      if (kt + 1 < n_tiles) load_tile(kt + 1);
-      if constexpr (MODE == 0) process_tile(buf, kt * BN, std::false_type{});
-      if constexpr (MODE == 1) process_tile(buf, kt * BN, std::true_type{});
-      if (kt + 1 < n_tiles) store_tile(buf ^ 1);
+      if (kt + NSTAGE - 1 < n_tiles) issue_tile(kt + NSTAGE - 1);
+      const unsigned st = unsigned(kt) % NSTAGE;
+      if constexpr (MODE == 0) process_tile(st, kt * BN, std::false_type{});
+      if constexpr (MODE == 1) process_tile(st, kt * BN, std::true_type{});
+      wait_next(kt);
       __syncthreads();
     }
   };
@@ -560,31 +596,31 @@ hipError_t launch_bwd_t(const BwdArgs& a) {
   if (n_pairs > 0) {
     const int64_t blocks = (n_pairs * 16 + 255) / 256;
     hipLaunchKernelGGL((bwd_delta_kernel<D>), dim3(unsigned(blocks)), dim3(256), 0, a.stream,
-                       static_cast<const __bf16*>(a.dout), static_cast<const __bf16*>(a.o), a.delta, a.rows_end,
-                       a.n_heads, a.total_tokens);
+                       static_cast<const __bf16*>(a.dout), static_cast<const __bf16*>(a.o), a.lse, a.ndelta,
+                       a.lse2, a.rows_end, a.n_heads, a.total_tokens);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   const KernelEvents& ev = kernel_events();
   if (a.n_units > 0) {
     if (ev.begin) (void)hipEventRecord(ev.begin, a.stream);
-    constexpr int NW = bwd_dkdv_waves(D);
-    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, NW, CAUSAL>), dim3(a.n_units), dim3(64 * NW), 0,
-                       a.stream, static_cast<const __bf16*>(a.q),
+    constexpr DkdvShape sh = bwd_dkdv_shape(D);
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, sh.kb, sh.waves, sh.stages, CAUSAL>), dim3(a.n_units), dim3(64 * sh.waves), 0, a.stream, static_cast<const __bf16*>(a.q),
                        static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
-                       static_cast<const __bf16*>(a.dout), a.lse, a.delta, static_cast<__bf16*>(a.dk),
-                       static_cast<__bf16*>(a.dv), static_cast<const WorkUnit*>(a.units), a.n_units / kNumXcd, a.n_heads,
-                       a.total_tokens, a.scale, a.scale * kLog2e);
+                       static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dk),
+                       static_cast<__bf16*>(a.dv), static_cast<const __bf16*>(a.consts),
+                       static_cast<const WorkUnit*>(a.units), a.n_units / kNumXcd, a.n_heads, a.total_tokens, a.scale,
+                       a.scale * kLog2e);
     hipError_t e = hipGetLastError();
     if (ev.end) (void)hipEventRecord(ev.end, a.stream);
     if (e != hipSuccess) return e;
   }
   if (a.n_qunits > 0) {
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, kBwdDqWaves, CAUSAL>), dim3(a.n_qunits),
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, kBwdDqWaves, (D > 96 ? 2 : 3), CAUSAL>), dim3(a.n_qunits),
                        dim3(64 * kBwdDqWaves), 0, a.stream, static_cast<const __bf16*>(a.q),
                        static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
-                       static_cast<const __bf16*>(a.dout), a.lse, a.delta, static_cast<__bf16*>(a.dq),
-                       static_cast<const WorkUnit*>(a.qunits), a.n_qunits / kNumXcd, a.n_heads, a.total_tokens, a.scale,
+                       static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dq),
+                       static_cast<const __bf16*>(a.consts), static_cast<const WorkUnit*>(a.qunits), a.n_qunits / kNumXcd, a.n_heads, a.total_tokens, a.scale,
                        a.scale * kLog2e);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -608,7 +644,10 @@ __global__ void fill_bf16_kernel(__bf16* p, int64_t n, uint32_t seed) {
 
 }  // namespace
 
-int bwd_key_tile_rows(int head_dim) { return 32 * bwd_dkdv_waves(head_dim); }
+int bwd_key_tile_rows(int head_dim) {
+  const DkdvShape sh = bwd_dkdv_shape(head_dim);
+  return 32 * sh.kb * sh.waves;
+}
 int bwd_query_tile_rows(int head_dim) { return 32 * kBwdDqWaves; }
 
 hipError_t launch_bwd(const BwdArgs& a) {

@@ -53,6 +53,19 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Wavefront issue priority around matrix-core phases: with two wavefronts
+// on a SIMD, the one feeding the matrix cores issues first and the other
+// fills the gaps with vector work.
+#ifndef DCP_MFMA_PRIO
+#define DCP_MFMA_PRIO 1
+#endif
+__device__ __forceinline__ void mfma_prio_hi() {
+  if (DCP_MFMA_PRIO) __builtin_amdgcn_s_setprio(1);
+}
+__device__ __forceinline__ void mfma_prio_lo() {
+  if (DCP_MFMA_PRIO) __builtin_amdgcn_s_setprio(0);
+}
+
 // Max / sum of a value with the lane 32 positions away (the two halves of a
 // wavefront), via the gfx950 cross-half lane swap.
 __device__ __forceinline__ float half_swap_max(float x) {
@@ -80,6 +93,22 @@ __device__ __forceinline__ bf16x8 cat(const bf16x4& lo, const bf16x4& hi) {
 }
 
 __device__ __forceinline__ bf16x8 lds_read_b128(const __bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
+
+// The same reads through LDS-address-space (32-bit) pointers.  Indexing a
+// __shared__ array through lds_ptr() keeps the address arithmetic in 32
+// bits, so constant terms fold into the instructions' offset fields.
+#define DCP_LDS __attribute__((address_space(3)))
+typedef DCP_LDS __bf16 lds_bf16;
+typedef DCP_LDS float lds_f32;
+template <typename T>
+__device__ __forceinline__ DCP_LDS T* lds_ptr(T* p) {
+  return (DCP_LDS T*)(p);
+}
+__device__ __forceinline__ bf16x4 lds_read_tr(const lds_bf16* p) {
+  return __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((DCP_LDS i16x4*)(p)));
+}
+__device__ __forceinline__ bf16x8 lds_read_b128(const lds_bf16* p) { return *(const DCP_LDS bf16x8*)(p); }
+__device__ __forceinline__ f32x4 lds_read_f32x4(const lds_f32* p) { return *(const DCP_LDS f32x4*)(p); }
 
 // Waits until at most N vector-memory operations of this wavefront are in
 // flight (gfx9 s_waitcnt: vmcnt split over bits 3:0 and 15:14; expcnt and
@@ -146,10 +175,39 @@ struct DmaTile {
   }
 };
 
+// Direct global -> LDS copy of N consecutive fp32 values (gfx9
+// global_load_lds_dword: each lane moves 4 bytes, a wavefront fills 256
+// consecutive LDS bytes).  Element e < valid comes from src[e], every other
+// element from the 4-byte constant at `fill`.  Like DmaTile, every
+// wavefront issues exactly NI instructions.
+template <int N, int NW>
+struct DmaVec {
+  static constexpr int NINS = N / 64;
+  static constexpr int NI = (NINS + NW - 1) / NW;
+  static_assert(N % 64 == 0, "vector must fill whole wavefront copies");
+
+  __device__ __forceinline__ static void issue(float* lds_vec, const float* src, int valid, const float* fill,
+                                               int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int t = min(wave + NW * i, NINS - 1);
+      const int e = 64 * t + lane;
+      const float* g = e < valid ? src + e : fill;
+      const uint32_t m0 = __builtin_amdgcn_readfirstlane(
+          static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds_vec + 64 * t)));
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"
+                   :
+                   : "s"(m0), "v"(reinterpret_cast<uint64_t>(g))
+                   : "memory");
+    }
+  }
+};
+
 // Offsets (bf16 elements) of the 16-byte constant chunks every attention
 // workspace starts with.
 constexpr int kConstZero = 0;   // [0, 0, 0, 0, 0, 0, 0, 0]
 constexpr int kConstOnes = 8;   // [1, 0, 0, 0, 0, 0, 0, 0]
+constexpr int kConstInf = 16;   // fp32 +inf (a query past its sequence end)
 constexpr int kConstBytes = 256;
 
 }  // namespace dcp

@@ -75,7 +75,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   const int h = u.head;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches on it
   const int g = lane >> 5;
   const int j = lane & 31;
   const int64_t ts = int64_t(H) * D;  // token stride

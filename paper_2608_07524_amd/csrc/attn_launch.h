@@ -15,22 +15,36 @@ namespace dcp {
 #endif
 constexpr int kFwdNQB = DCP_FWD_NQB;
 constexpr int kFwdWaves = DCP_FWD_WAVES;
-// Backward: kBwdWaves wavefronts per workgroup, 32 keys (dK/dV pass) or 32
-// queries (dQ pass) each; the dK/dV pass steps over kBwdBM queries at a
-// time, the dQ pass over kBwdDqBN keys.
-// The dK/dV pass keeps K, V fragments and dK, dV accumulators resident; at
-// head width 128 they do not fit the 256 registers of two wavefronts per
-// SIMD, so that width runs one wavefront per SIMD.
-#ifndef DCP_BWD_WAVES_D128
-#define DCP_BWD_WAVES_D128 4
+// Backward, dK/dV pass: `waves` wavefronts per workgroup, each owning
+// 32*kb keys whose K, V fragments and dK, dV accumulators stay resident,
+// stepping over kBwdBM queries at a time through a `stages`-deep LDS ring.
+// Head widths up to 72 run two wavefronts of 32 keys per SIMD.  At head
+// width 128 the resident state needs more than the 256 registers two
+// wavefronts per SIMD could each have, so that width runs one wavefront per
+// SIMD, and its ring holds two stages (three do not fit the 160 KB of LDS).
+// dQ pass: kBwdDqWaves wavefronts of 32 queries, kBwdDqBN keys per step.
+struct DkdvShape {
+  int kb, waves, stages;
+};
+#ifndef DCP_DKDV_KB
+#define DCP_DKDV_KB 1
 #endif
-#ifndef DCP_BWD_WAVES
-#define DCP_BWD_WAVES 8
+#ifndef DCP_DKDV_WAVES
+#define DCP_DKDV_WAVES 8
+#endif
+#ifndef DCP_DKDV_KB_D128
+#define DCP_DKDV_KB_D128 1
+#endif
+#ifndef DCP_DKDV_WAVES_D128
+#define DCP_DKDV_WAVES_D128 4
 #endif
 #ifndef DCP_BWD_DQ_WAVES
 #define DCP_BWD_DQ_WAVES 8
 #endif
-constexpr int bwd_dkdv_waves(int head_dim) { return head_dim > 96 ? DCP_BWD_WAVES_D128 : DCP_BWD_WAVES; }
+constexpr DkdvShape bwd_dkdv_shape(int head_dim) {
+  return head_dim > 96 ? DkdvShape{DCP_DKDV_KB_D128, DCP_DKDV_WAVES_D128, 2}
+                       : DkdvShape{DCP_DKDV_KB, DCP_DKDV_WAVES, 3};
+}
 constexpr int kBwdDqWaves = DCP_BWD_DQ_WAVES;
 constexpr int kBwdBM = 64;
 constexpr int kBwdDqBN = 64;
@@ -62,7 +76,9 @@ struct BwdArgs {
   void* dq;
   void* dk;
   void* dv;
-  float* delta;           // fp32 [H, T] workspace
+  float* ndelta;          // fp32 [H, T] workspace: -rowsum(dO o O)
+  float* lse2;            // fp32 [H, T] workspace: LSE * log2(e)
+  const void* consts;     // device: the 16-byte constant chunks (workspace head)
   const void* units;      // device WorkUnit[n_units], key tiles (8 per-die lists)
   int n_units;
   const void* qunits;     // device WorkUnit[n_qunits], query tiles (8 per-die lists)

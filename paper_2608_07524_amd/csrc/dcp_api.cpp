@@ -6,8 +6,11 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
+#include <limits>
 #include <mutex>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "attn_common.h"
@@ -169,33 +172,38 @@ size_t count_units(const dcp_attn_desc* d, int tile) {
   return tiles_per_head(d, tile) * size_t(d->n_heads) * kNumXcd;
 }
 
+// Backward workspace: constant chunks | key-tile list | query-tile list |
+// LSE*log2e [H, T] | Delta [H, T].
 struct BwdLayout {
-  size_t delta, units, qunits, total;
+  size_t units, qunits, lse2, delta, total;
 };
 BwdLayout bwd_layout(const dcp_attn_desc* d) {
+  const size_t per_row = align_up(size_t(4) * size_t(d->n_heads) * size_t(d->total_tokens));
   BwdLayout l;
-  l.delta = 0;
-  l.units = align_up(size_t(4) * size_t(d->n_heads) * size_t(d->total_tokens));
+  l.units = kConstBytes;
   l.qunits = l.units + align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, bwd_key_tile_rows(d->head_dim))));
-  l.total = l.qunits + align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, bwd_query_tile_rows(d->head_dim))));
+  l.lse2 = l.qunits + align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, bwd_query_tile_rows(d->head_dim))));
+  l.delta = l.lse2 + per_row;
+  l.total = l.delta + per_row;
   return l;
 }
 
-int upload_units(const std::vector<WorkUnit>& units, void* dst, hipStream_t stream) {
-  if (units.empty()) return DCP_OK;
-  hipError_t e = hipMemcpyAsync(dst, units.data(), units.size() * sizeof(WorkUnit), hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
-  return DCP_OK;
-}
-
-// The constant block at the head of a workspace, followed by a work list,
-// uploaded with one copy: 16-byte chunks the kernels' direct-to-LDS copies
-// read for pad columns ([0 x 8] and [1, 0 x 7] in bf16).
-int upload_consts_and_units(const std::vector<WorkUnit>& units, void* dst, hipStream_t stream) {
-  std::vector<unsigned char> buf(kConstBytes + units.size() * sizeof(WorkUnit), 0);
+// The constant block at the head of a workspace -- 16-byte chunks the
+// kernels' direct-to-LDS copies read for pad columns ([0 x 8] and
+// [1, 0 x 7] in bf16) and for rows past a sequence end (fp32 +inf) --
+// and the work lists after it, uploaded with one copy.  Each list goes to
+// its byte offset in the workspace.
+int upload_head(std::initializer_list<std::pair<size_t, const std::vector<WorkUnit>*>> lists, void* dst,
+                hipStream_t stream) {
+  size_t bytes = kConstBytes;
+  for (const auto& l : lists) bytes = std::max(bytes, l.first + l.second->size() * sizeof(WorkUnit));
+  std::vector<unsigned char> buf(bytes, 0);
   const uint16_t one = 0x3F80;  // bf16 1.0
   std::memcpy(buf.data() + kConstOnes * 2, &one, sizeof one);
-  if (!units.empty()) std::memcpy(buf.data() + kConstBytes, units.data(), units.size() * sizeof(WorkUnit));
+  const float inf = std::numeric_limits<float>::infinity();
+  std::memcpy(buf.data() + kConstInf * 2, &inf, sizeof inf);
+  for (const auto& l : lists)
+    if (!l.second->empty()) std::memcpy(buf.data() + l.first, l.second->data(), l.second->size() * sizeof(WorkUnit));
   hipError_t e = hipMemcpyAsync(dst, buf.data(), buf.size(), hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
   return DCP_OK;
@@ -258,7 +266,7 @@ extern "C" int dcp_varlen_attn_fwd(const dcp_attn_desc* desc, const void* q, con
   const std::vector<WorkUnit> units = build_units(desc, tile, false);
   if (units.empty()) return DCP_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = upload_consts_and_units(units, workspace, s))) return st;
+  if ((st = upload_head({{kConstBytes, &units}}, workspace, s))) return st;
   char* ws = static_cast<char*>(workspace);
   FwdArgs a{q, k, v, o, lse, ws, ws + kConstBytes, int(units.size()), desc->n_heads, desc->head_dim,
             int(desc->total_tokens), desc->scale, desc->causal, s};
@@ -288,10 +296,10 @@ extern "C" int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, 
   const std::vector<WorkUnit> qunits = build_units(desc, bwd_query_tile_rows(desc->head_dim), false);
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
-  if ((st = upload_units(units, ws + l.units, s))) return st;
-  if ((st = upload_units(qunits, ws + l.qunits, s))) return st;
+  if ((st = upload_head({{l.units, &units}, {l.qunits, &qunits}}, workspace, s))) return st;
   BwdArgs a{dout, o, lse, q, k, v, dq, dk, dv, reinterpret_cast<float*>(ws + l.delta),
-            ws + l.units, int(units.size()), ws + l.qunits, int(qunits.size()),
+            reinterpret_cast<float*>(ws + l.lse2), ws, ws + l.units, int(units.size()), ws + l.qunits,
+            int(qunits.size()),
             desc->cu_seqlens_host[desc->n_seqs], desc->n_heads, desc->head_dim, int(desc->total_tokens),
             desc->scale, desc->causal, s};
   hipError_t e = launch_bwd(a);
