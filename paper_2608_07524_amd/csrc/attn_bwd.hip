@@ -33,6 +33,8 @@
 #include "attn_common.h"
 #include "attn_launch.h"
 
+
+
 namespace dcp {
 namespace {
 
@@ -132,8 +134,8 @@ __device__ __forceinline__ void store_rows_bf16(const f32x16 (&acc)[NDB], float 
 // dP - Delta directly.  With KB = 2 every operand fetched from LDS feeds
 // two matrix products, and the exponentials of one key block can overlap
 // the products of the other.
-template <int D, int KB, int NW, int NSTAGE, bool CAUSAL>
-__global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_kernel(
+template <int D, int KB, int NW, int BM, int NSTAGE, int WPE, bool CAUSAL>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) void attn_bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
     __bf16* __restrict__ dk, __bf16* __restrict__ dv, const __bf16* __restrict__ consts,
@@ -142,12 +144,12 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_kernel(
   constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
   constexpr int RSTR = S::DP + 8;  // an odd number of 16-byte chunks
   constexpr int TSTR = S::TSTR;
-  constexpr int BM = kBwdBM;  // queries per tile
+  static_assert(BM % 32 == 0, "whole 32-query blocks per tile");
   using DR = DmaTile<BM, RSTR / 8, CPR, NW>;
   using DT = DmaTile<BM, TSTR / 8, CPR, NW>;
-  using DL = DmaVec<BM, NW>;
-  constexpr int NI = 2 * DR::NI + 2 * DT::NI + 2 * DL::NI;  // copies per wavefront per tile
-  constexpr int RBUF = BM * RSTR, TBUF = BM * TSTR;
+  using DL = DmaVecPair<BM, NW>;
+  constexpr int NI = 2 * DR::NI + 2 * DT::NI + DL::NI;  // copies per wavefront per tile
+  constexpr int RBUF = DR::ELEMS, TBUF = DT::ELEMS;
   constexpr int SSTR = S::RSTR;  // epilogue staging stride
   __shared__ __attribute__((aligned(16))) __bf16 Qr[NSTAGE * RBUF];
   __shared__ __attribute__((aligned(16))) __bf16 dOr[NSTAGE * RBUF];
@@ -217,8 +219,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_kernel(
     DR::issue(&dOr[st * RBUF], ds, ts, valid, zero, zero, wave, lane);
     DT::issue(&dOt[st * TBUF], ds, ts, valid, zero, zero, wave, lane);
     // A query past the sequence end gets LSE = +inf, so its P is exactly 0.
-    DL::issue(&LV[st * 2 * BM], lseh + q0, valid, finf, wave, lane);
-    DL::issue(&LV[st * 2 * BM + BM], ndh + q0, valid, fzero, wave, lane);
+    DL::issue(&LV[st * 2 * BM], lseh + q0, ndh + q0, valid, finf, fzero, wave, lane);
   };
   // Waits until tile it+1 has landed (tile it+2 may stay in flight).
   auto wait_next = [&](int it) {
@@ -605,7 +606,7 @@ hipError_t launch_bwd_t(const BwdArgs& a) {
   if (a.n_units > 0) {
     if (ev.begin) (void)hipEventRecord(ev.begin, a.stream);
     constexpr DkdvShape sh = bwd_dkdv_shape(D);
-    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, sh.kb, sh.waves, sh.stages, CAUSAL>), dim3(a.n_units), dim3(64 * sh.waves), 0, a.stream, static_cast<const __bf16*>(a.q),
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, sh.kb, sh.waves, sh.bm, sh.stages, sh.waves_per_eu, CAUSAL>), dim3(a.n_units), dim3(64 * sh.waves), 0, a.stream, static_cast<const __bf16*>(a.q),
                        static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
                        static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dk),
                        static_cast<__bf16*>(a.dv), static_cast<const __bf16*>(a.consts),

@@ -125,17 +125,19 @@ __device__ __forceinline__ void wait_vmcnt() {
 // (r, c) of the tile sits at byte 16*(r*CPR_PAD + c); slots c < CPR_DATA of
 // rows r < valid_rows come from src + r*row_stride + 8c, slot c == CPR_DATA
 // from `first_pad` (a 16-byte constant chunk, e.g. [1, 0, ..., 0] for a
-// row-sum column) and every other slot from `zero`.  Every wavefront issues
-// exactly NI instructions per tile (the last one repeated when the tile
-// does not split evenly; the repeat rewrites identical bytes), so a fixed
-// wait_vmcnt count covers the tile on every wavefront.  Completion is
-// tracked by vmcnt only: wait, then barrier, before reading the tile.
+// row-sum column) and every other slot from `zero`.  The tile occupies
+// ELEMS = 512*NINS elements: when ROWS*CPR_PAD is not a multiple of 64,
+// the last copy also fills the slots past the tile with zeros.  Every
+// wavefront issues exactly NI instructions per tile (the last one repeated
+// when they do not split evenly; the repeat rewrites identical bytes), so
+// a fixed wait_vmcnt count covers the tile on every wavefront.  Completion
+// is tracked by vmcnt only: wait, then barrier, before reading the tile.
 template <int ROWS, int CPR_PAD, int CPR_DATA, int NW>
 struct DmaTile {
   static constexpr int NSLOT = ROWS * CPR_PAD;
-  static constexpr int NINS = NSLOT / 64;
+  static constexpr int NINS = (NSLOT + 63) / 64;
   static constexpr int NI = (NINS + NW - 1) / NW;
-  static_assert(NSLOT % 64 == 0, "tile must fill whole wavefront copies");
+  static constexpr int ELEMS = 512 * NINS;
   static_assert(CPR_DATA < CPR_PAD, "pad slots hold the constant chunks");
 
   __device__ __forceinline__ static void issue(__bf16* lds_tile, const __bf16* src, int64_t row_stride,
@@ -148,8 +150,8 @@ struct DmaTile {
       const int r = slot / CPR_PAD, c = slot % CPR_PAD;
       const __bf16* g = zero;
       if (c < CPR_DATA) {
-        if (r < valid_rows) g = src + int64_t(r) * row_stride + 8 * c;
-      } else if (c == CPR_DATA) {
+        if (r < valid_rows && r < ROWS) g = src + int64_t(r) * row_stride + 8 * c;
+      } else if (c == CPR_DATA && r < ROWS) {
         g = first_pad;
       }
       dma16(g, lds_tile + 512 * t);
@@ -175,24 +177,27 @@ struct DmaTile {
   }
 };
 
-// Direct global -> LDS copy of N consecutive fp32 values (gfx9
-// global_load_lds_dword: each lane moves 4 bytes, a wavefront fills 256
-// consecutive LDS bytes).  Element e < valid comes from src[e], every other
-// element from the 4-byte constant at `fill`.  Like DmaTile, every
-// wavefront issues exactly NI instructions.
+// Direct global -> LDS copy of two N-element fp32 vectors stored back to
+// back (gfx9 global_load_lds_dword: each lane moves 4 bytes, a wavefront
+// fills 256 consecutive LDS bytes).  Element e < valid of the first vector
+// comes from a[e], of the second from b[e]; every other element from the
+// 4-byte constant at fill_a / fill_b.  Like DmaTile, every wavefront
+// issues exactly NI instructions.
 template <int N, int NW>
-struct DmaVec {
-  static constexpr int NINS = N / 64;
+struct DmaVecPair {
+  static constexpr int NINS = 2 * N / 64;
   static constexpr int NI = (NINS + NW - 1) / NW;
-  static_assert(N % 64 == 0, "vector must fill whole wavefront copies");
+  static_assert(2 * N % 64 == 0, "vectors must fill whole wavefront copies");
 
-  __device__ __forceinline__ static void issue(float* lds_vec, const float* src, int valid, const float* fill,
-                                               int wave, int lane) {
+  __device__ __forceinline__ static void issue(float* lds_vec, const float* a, const float* b, int valid,
+                                               const float* fill_a, const float* fill_b, int wave, int lane) {
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int t = min(wave + NW * i, NINS - 1);
       const int e = 64 * t + lane;
-      const float* g = e < valid ? src + e : fill;
+      const bool second = e >= N;
+      const int idx = second ? e - N : e;
+      const float* g = idx < valid ? (second ? b : a) + idx : (second ? fill_b : fill_a);
       const uint32_t m0 = __builtin_amdgcn_readfirstlane(
           static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds_vec + 64 * t)));
       asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"

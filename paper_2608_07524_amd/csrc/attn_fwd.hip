@@ -118,7 +118,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   const int n_tiles = (key_end + BN - 1) / BN;
 
   auto issue_tile = [&](int kt) {
-    const int st = kt % 3;
+    const unsigned st = unsigned(kt) % 3;
     const int valid = min(BN, seqlen - kt * BN);
     DK::issue(&Ks[st * KBUF], kh + int64_t(kt) * BN * ts, ts, valid, zero, zero, wave, lane);
     DV::issue(&Vs[st * VBUF], vh + int64_t(kt) * BN * ts, ts, valid, zero, v_pad, wave, lane);
@@ -151,15 +151,20 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   const int wave_last_q = wave_q0 + QPW - 1;
   // transposing-read addressing (see lds_read_tr): this lane's element
   // offset inside a V tile; every other term is a compile-time constant
-  const int tr_off = (4 * g + ((lane & 15) >> 2)) * VSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const unsigned tr_off = (4 * g + ((lane & 15) >> 2)) * VSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   // and the 16-byte read offset inside a K tile
-  const int kr_off = j * KSTR + 8 * g;
+  const unsigned kr_off = j * KSTR + 8 * g;
+  const lds_bf16* Ks3 = lds_ptr(Ks);
+  const lds_bf16* Vs3 = lds_ptr(Vs);
 
   // One key tile.  MASK selects the variant for tiles that reach past the
   // sequence end or cross the causal diagonal; it is a compile-time flag so
   // the common unmasked tiles carry no per-element compare and select.
-  auto process_tile = [&](const __bf16* Kb, const __bf16* Vb, int k0, auto mask_tag) {
+  auto process_tile = [&](unsigned st, int k0, auto mask_tag) {
     constexpr bool MASK = decltype(mask_tag)::value;
+    unsigned kb0 = st * KBUF + kr_off;
+    unsigned vb0 = st * VBUF + tr_off;
+    asm("" : "+v"(kb0), "+v"(vb0));  // keeps the constant terms in the offset fields
     f32x16 s[2][NQB];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -169,7 +174,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
     for (int kd = 0; kd < NKD; ++kd) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8 a = lds_read_b128(Kb + kr_off + 32 * kb * KSTR + 16 * kd);
+        const bf16x8 a = lds_read_b128(Ks3 + kb0 + 32 * kb * KSTR + 16 * kd);
 #pragma unroll
         for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = mfma32(a, qf[qb][kd], s[kb][qb]);
       }
@@ -240,7 +245,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
           // keys 32kb + 16hh + 4g + {0..3} and + 8 + {0..3}; column 32db + (lane % 32)
-          const __bf16* p = Vb + tr_off + (32 * kb + 16 * hh) * VSTR + 32 * db;
+          const lds_bf16* p = Vs3 + vb0 + (32 * kb + 16 * hh) * VSTR + 32 * db;
           const bf16x8 a = cat(lds_read_tr(p), lds_read_tr(p + 8 * VSTR));
 #pragma unroll
           for (int qb = 0; qb < NQB; ++qb) oacc[qb][db] = mfma32(a, pb[kb][hh][qb], oacc[qb][db]);
@@ -264,10 +269,10 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   auto run = [&](int kt0, int kt1, auto mode_tag) {
     constexpr int MODE = decltype(mode_tag)::value;  // 0 unmasked, 1 masked, 2 idle
     for (int kt = kt0; kt < kt1; ++kt) {
-      const int st = kt % 3;
+      const unsigned st = unsigned(kt) % 3;
       if (kt + 2 < n_tiles) issue_tile(kt + 2);
-      if constexpr (MODE == 0) process_tile(&Ks[st * KBUF], &Vs[st * VBUF], kt * BN, std::false_type{});
-      if constexpr (MODE == 1) process_tile(&Ks[st * KBUF], &Vs[st * VBUF], kt * BN, std::true_type{});
+      if constexpr (MODE == 0) process_tile(st, kt * BN, std::false_type{});
+      if constexpr (MODE == 1) process_tile(st, kt * BN, std::true_type{});
       wait_next(kt);
       __syncthreads();
     }

@@ -17,20 +17,27 @@ constexpr int kFwdNQB = DCP_FWD_NQB;
 constexpr int kFwdWaves = DCP_FWD_WAVES;
 // Backward, dK/dV pass: `waves` wavefronts per workgroup, each owning
 // 32*kb keys whose K, V fragments and dK, dV accumulators stay resident,
-// stepping over kBwdBM queries at a time through a `stages`-deep LDS ring.
+// stepping over `bm` queries at a time through a `stages`-deep LDS ring;
+// waves_per_eu is the occupancy the register allocation must allow.
 // Head widths up to 72 run two wavefronts of 32 keys per SIMD.  At head
 // width 128 the resident state needs more than the 256 registers two
 // wavefronts per SIMD could each have, so that width runs one wavefront per
 // SIMD, and its ring holds two stages (three do not fit the 160 KB of LDS).
 // dQ pass: kBwdDqWaves wavefronts of 32 queries, kBwdDqBN keys per step.
 struct DkdvShape {
-  int kb, waves, stages;
+  int kb, waves, bm, stages, waves_per_eu;
 };
 #ifndef DCP_DKDV_KB
 #define DCP_DKDV_KB 1
 #endif
 #ifndef DCP_DKDV_WAVES
 #define DCP_DKDV_WAVES 8
+#endif
+#ifndef DCP_DKDV_BM
+#define DCP_DKDV_BM 64
+#endif
+#ifndef DCP_DKDV_WPE
+#define DCP_DKDV_WPE 2
 #endif
 #ifndef DCP_DKDV_KB_D128
 #define DCP_DKDV_KB_D128 1
@@ -42,11 +49,10 @@ struct DkdvShape {
 #define DCP_BWD_DQ_WAVES 8
 #endif
 constexpr DkdvShape bwd_dkdv_shape(int head_dim) {
-  return head_dim > 96 ? DkdvShape{DCP_DKDV_KB_D128, DCP_DKDV_WAVES_D128, 2}
-                       : DkdvShape{DCP_DKDV_KB, DCP_DKDV_WAVES, 3};
+  return head_dim > 96 ? DkdvShape{DCP_DKDV_KB_D128, DCP_DKDV_WAVES_D128, 64, 2, 1}
+                       : DkdvShape{DCP_DKDV_KB, DCP_DKDV_WAVES, DCP_DKDV_BM, 3, DCP_DKDV_WPE};
 }
 constexpr int kBwdDqWaves = DCP_BWD_DQ_WAVES;
-constexpr int kBwdBM = 64;
 constexpr int kBwdDqBN = 64;
 
 struct FwdArgs {
