@@ -53,6 +53,13 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// v_mfma_f32_16x16x32_bf16: lane (g4, i), g4 = lane / 16, holds row i of
+// A (16 x 32) and column i of B (32 x 16) with the 8 contraction indices of
+// group g4; C/D lane (g4, i), register r holds row 4*g4 + r, column i.
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
 // Wavefront issue priority around matrix-core phases: with two wavefronts
 // on a SIMD, the one feeding the matrix cores issues first and the other
 // fills the gaps with vector work.

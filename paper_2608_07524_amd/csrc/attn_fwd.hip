@@ -5,13 +5,17 @@
 // Work decomposition: one workgroup per (query tile, head).  A query tile
 // never straddles two sequences, and the key loop runs over the tile's own
 // sequence only, so no off-diagonal (cross-sequence) block is ever touched.
-// NW wavefronts per workgroup, each owning 32*NQB query rows.
+// NW wavefronts per workgroup, each owning 32 query rows.
 //
-// Per key tile of BN = 64 keys (a three-stage LDS ring filled by direct
-// global-to-LDS copies two tiles ahead; one barrier per tile):
+// Keys arrive in tiles of BN = 64 rows through a four-stage LDS ring filled
+// by direct global-to-LDS copies three tiles ahead (one barrier per tile).
+// Each wavefront walks its keys in blocks of 32 and software-pipelines them:
+// while the exponentials of block b run on the vector ALUs, the matrix cores
+// compute the scores of block b + 1, and while block b's probabilities are
+// multiplied into O, the vector ALUs take block b + 1's row maximum.
 //   S^T = K Q^T      A = K rows from LDS, B = Q rows kept in registers;
-//                    each lane ends up holding one query and 16 keys.
-//   m, P             row max: in-lane over 32 keys + one cross-half swap;
+//                    each lane holds one query and 16 keys of the block.
+//   m, P             row max: in-lane over 16 keys + one cross-half swap;
 //                    P = exp2(S*scale*log2e - m) stays in registers.
 //   O^T += V^T P^T   A = V^T via transposing LDS reads of the row-major V
 //                    tile, B = P^T straight from the S^T accumulator layout.
@@ -31,6 +35,15 @@ namespace dcp {
 namespace {
 
 constexpr int kFwdBN = 64;
+#ifndef DCP_FWD_STAGES
+#define DCP_FWD_STAGES 4
+#endif
+#ifndef DCP_FWD_SCHED
+#define DCP_FWD_SCHED 0
+#endif
+// Ring depth: tile kt + kFwdStages - 1 streams in while tile kt is consumed.
+constexpr int kFwdStages = DCP_FWD_STAGES;
+static_assert(kFwdStages >= 3, "tiles kt and kt + 1 are read while kt + 2 lands");
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 
 template <int D>
@@ -46,9 +59,20 @@ struct FwdShape {
   static constexpr int VW = NDB * 32;
   static constexpr int VSTR = (VW % 64 == 32) ? VW : VW + 32;
   static constexpr int CPR = D / 8;  // 16-byte chunks per row
+  // When 16-row blocks cover D plus the row-sum row with fewer padded rows
+  // than 32-row blocks do (D = 72: 80 rows instead of 96), O^T is built
+  // from 16x16x32 products instead.
+  static constexpr int NMB = (D + 1 + 15) / 16;
+  static constexpr bool PV16 = ONES_ROW && NMB * 16 < NDB * 32;
 };
 
-template <int D, int NQB, int NW, bool CAUSAL>
+// Interleaving hints for the compiler's scheduler (masks of
+// __builtin_amdgcn_sched_group_barrier).
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedValu = 0x002;
+constexpr int kSchedDsRead = 0x100;
+
+template <int D, int NW, bool CAUSAL>
 __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restrict__ q,
                                                            const __bf16* __restrict__ k,
                                                            const __bf16* __restrict__ v, __bf16* __restrict__ o,
@@ -59,16 +83,16 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   using S = FwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, KSTR = S::KSTR, VSTR = S::VSTR, CPR = S::CPR;
   constexpr int BN = kFwdBN;
-  constexpr int NT = 64 * NW;  // threads
-  constexpr int QPW = 32 * NQB;
   constexpr int KBUF = BN * KSTR, VBUF = BN * VSTR;
+  // as deep as asked, within the 160 KB of LDS
+  constexpr int NST = kFwdStages * 2 * (KBUF + VBUF) <= 163840 ? kFwdStages : 163840 / (2 * (KBUF + VBUF));
+  static_assert(NST >= 3, "ring too shallow");
   using DK = DmaTile<BN, KSTR / 8, CPR, NW>;
   using DV = DmaTile<BN, VSTR / 8, CPR, NW>;
   constexpr int NI = DK::NI + DV::NI;  // copies per wavefront per tile
 
-  // Three-stage ring: tile kt+2 streams in while tile kt is consumed.
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[3 * KBUF];
-  __shared__ __attribute__((aligned(16))) __bf16 Vs[3 * VBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[NST * KBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[NST * VBUF];
 
   const WorkUnit u = unit_for_block(units, per_xcd);
   if (u.rows == 0) return;
@@ -88,24 +112,21 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   // column holds ones when it is the row-sum column.
   const __bf16* v_pad = S::ONES_ROW ? consts + kConstOnes : zero;
 
-  const int tile_q0 = u.row0 - u.seq0;       // first query of the tile, sequence-relative
-  const int wave_q0 = tile_q0 + wave * QPW;  // first query of this wave
+  const int tile_q0 = u.row0 - u.seq0;  // first query of the tile, sequence-relative
+  const int wave_q0 = tile_q0 + wave * 32;
   const int seqlen = u.seqlen;
+  const int qi = wave_q0 + j;  // this lane's query
 
-  // Q fragments (B operand of S^T): lane (g, j) holds query j of each
-  // 32-row block, columns 16*kd + 8*g .. +7.
-  bf16x8 qf[NQB][NKD];
+  // Q fragments (B operand of S^T): lane (g, j) holds query j,
+  // columns 16*kd + 8*g .. +7.
+  bf16x8 qf[NKD];
 #pragma unroll
-  for (int qb = 0; qb < NQB; ++qb) {
-    const int qrel = wave * QPW + 32 * qb + j;  // row within the tile
-#pragma unroll
-    for (int kd = 0; kd < NKD; ++kd) {
-      const int col = 16 * kd + 8 * g;
-      if (qrel < u.rows && col < D) {
-        qf[qb][kd] = *reinterpret_cast<const bf16x8*>(qh + int64_t(tile_q0 + qrel) * ts + col);
-      } else {
-        qf[qb][kd] = bf16x8{};
-      }
+  for (int kd = 0; kd < NKD; ++kd) {
+    const int col = 16 * kd + 8 * g;
+    if (wave * 32 + j < u.rows && col < D) {
+      qf[kd] = *reinterpret_cast<const bf16x8*>(qh + int64_t(qi) * ts + col);
+    } else {
+      qf[kd] = bf16x8{};
     }
   }
 
@@ -116,214 +137,292 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
 
   const int key_end = CAUSAL ? min(seqlen, tile_q0 + u.rows) : seqlen;
   const int n_tiles = (key_end + BN - 1) / BN;
+  // This wavefront's 32-key blocks.  Blocks from b_mask on cross the
+  // sequence end or the causal diagonal (only ever the last one or two);
+  // blocks before it need no mask.  The wavefront works through whole
+  // tiles: t_plain tiles whose blocks and successors are all unmasked, then
+  // up to t_work tiles with masking on (a block past the wavefront's keys is
+  // simply fully masked), then idles to n_tiles so that every wavefront
+  // meets the same barriers.  A wavefront holding no query of the tile
+  // computes on zero queries; its rows are never stored.
+  const int wave_keys = CAUSAL ? min(seqlen, wave_q0 + 32) : seqlen;
+  const int nb = min((wave_keys + 31) / 32, 2 * n_tiles);
+  const int b_mask = min(nb, CAUSAL ? min(seqlen / 32, (wave_q0 + 1) / 32) : seqlen / 32);
+  const int t_work = (nb + 1) / 2;
+  const int t_plain = b_mask >= 1 ? (b_mask - 1) / 2 : 0;  // tiles kt with 2kt + 2 < b_mask
 
   auto issue_tile = [&](int kt) {
-    const unsigned st = unsigned(kt) % 3;
+    const unsigned st = unsigned(kt) % NST;
     const int valid = min(BN, seqlen - kt * BN);
     DK::issue(&Ks[st * KBUF], kh + int64_t(kt) * BN * ts, ts, valid, zero, zero, wave, lane);
     DV::issue(&Vs[st * VBUF], vh + int64_t(kt) * BN * ts, ts, valid, zero, v_pad, wave, lane);
   };
-  // Before the barrier that ends tile kt: tile kt+1 must have landed; only
-  // tile kt+2's copies (issued this iteration) may still be in flight.
-  auto wait_next = [&](int kt) {
-    if (kt + 2 < n_tiles) {
+  // Before tile kt is consumed, tiles kt and kt + 1 must have landed (the
+  // scores of tile kt + 1's first block are computed while tile kt is
+  // processed); copies of the tiles after them may still be in flight.
+  constexpr int PD = NST - 1;  // prefetch distance in tiles
+  auto wait_for = [&](int kt) {
+    const int ahead = min(PD - 2, n_tiles - kt - 2);  // tiles issued beyond kt + 1
+    if (PD >= 4 && ahead >= 2) {
+      wait_vmcnt<(PD >= 4 ? 2 * NI : 0)>();
+    } else if (PD >= 3 && ahead >= 1) {
       wait_vmcnt<NI>();
     } else {
       wait_vmcnt<0>();
     }
   };
 
-  float m_use[NQB], l_run[NQB];
-  f32x16 oacc[NQB][NDB];
-#pragma unroll
-  for (int qb = 0; qb < NQB; ++qb) {
-    m_use[qb] = -INFINITY;
-    l_run[qb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) oacc[qb][db] = f32x16{};
-  }
-
-  if (n_tiles > 0) issue_tile(0);
-  if (n_tiles > 1) issue_tile(1);
-  wait_next(-1);
-  __syncthreads();
-
-  const int wave_last_q = wave_q0 + QPW - 1;
   // transposing-read addressing (see lds_read_tr): this lane's element
   // offset inside a V tile; every other term is a compile-time constant
   const unsigned tr_off = (4 * g + ((lane & 15) >> 2)) * VSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  // (16x16x32 products: lane group g4 = lane / 16 reads the key runs
+  // starting at 0, 16, 4, 20 and 8 further, see pv_product)
+  const int g4 = lane >> 4;
+  const unsigned tr16_off = (16 * (g4 & 1) + 4 * (g4 >> 1) + ((lane & 15) >> 2)) * VSTR + 4 * (lane & 3);
+  const unsigned tr_lane = S::PV16 ? tr16_off : tr_off;
   // and the 16-byte read offset inside a K tile
   const unsigned kr_off = j * KSTR + 8 * g;
   const lds_bf16* Ks3 = lds_ptr(Ks);
   const lds_bf16* Vs3 = lds_ptr(Vs);
 
-  // One key tile.  MASK selects the variant for tiles that reach past the
-  // sequence end or cross the causal diagonal; it is a compile-time flag so
-  // the common unmasked tiles carry no per-element compare and select.
-  auto process_tile = [&](unsigned st, int k0, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    unsigned kb0 = st * KBUF + kr_off;
-    unsigned vb0 = st * VBUF + tr_off;
-    asm("" : "+v"(kb0), "+v"(vb0));  // keeps the constant terms in the offset fields
-    f32x16 s[2][NQB];
+  float m_use = -INFINITY, l_run = 0.f;
+  f32x16 oacc[NDB];  // O^T in 32-row blocks (lane (g, j): query j)
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+  for (int db = 0; db < NDB; ++db) oacc[db] = f32x16{};
+  // or, when PV16, in 16x16 blocks: [d block][query block]; lane (g4, n)
+  // holds query 16 * qb + n, rows 16 * mb + 4 * g4 + {0..3}
+  constexpr int NMB = S::NMB;
+  f32x4 oacc16[NMB][2];
 #pragma unroll
-      for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = f32x16{};
+  for (int mb = 0; mb < NMB; ++mb) oacc16[mb][0] = oacc16[mb][1] = f32x4{};
+
+  // S^T of one 32-key block whose K rows start at LDS element kbase.
+  auto scores = [&](unsigned kbase) {
+    f32x16 s = f32x16{};
 #pragma unroll
-    for (int kd = 0; kd < NKD; ++kd) {
+    for (int kd = 0; kd < NKD; ++kd) s = mfma32(lds_read_b128(Ks3 + kbase + 16 * kd), qf[kd], s);
+    return s;
+  };
+  auto apply_mask = [&](f32x16& s, int b) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8 a = lds_read_b128(Ks3 + kb0 + 32 * kb * KSTR + 16 * kd);
-#pragma unroll
-        for (int qb = 0; qb < NQB; ++qb) s[kb][qb] = mfma32(a, qf[qb][kd], s[kb][qb]);
-      }
+    for (int r = 0; r < 16; ++r) {
+      const int key = 32 * b + 8 * (r >> 2) + 4 * g + (r & 3);
+      if (key >= seqlen || (CAUSAL && key > qi)) s[r] = -INFINITY;
     }
-    if constexpr (MASK) {
+  };
+  auto row_max = [&](const f32x16& s) {
+    float t = -INFINITY;  // a sequential chain lowers to v_max3
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+    for (int r = 0; r < 16; ++r) t = fmaxf(t, s[r]);
+    return half_swap_max(t) * scale_log2;
+  };
+  // Lazy rescale: move m only when the row max outgrows it by > 2^8.
+  auto rescale = [&](float mx, bool valid) {
+    if (__builtin_amdgcn_ballot_w64(valid && mx > m_use + kRescaleSlack)) {
+      const float m_new = fmaxf(m_use, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_use - m_new);  // 0 on the first block
+      m_use = m_new;
+      l_run *= alpha;
+      if constexpr (S::PV16) {
+        // alpha of queries n and 16 + n for lane (g4, n)
+        auto sw = __builtin_amdgcn_permlane16_swap(__float_as_uint(alpha), __float_as_uint(alpha), false, false);
+        const float a0 = __uint_as_float(sw[0]), a1 = __uint_as_float(sw[1]);
 #pragma unroll
-        for (int qb = 0; qb < NQB; ++qb) {
-          const int qi = wave_q0 + 32 * qb + j;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * g + (r & 3);
-            if (key >= seqlen || (CAUSAL && key > qi)) s[kb][qb][r] = -INFINITY;
-          }
+        for (int mb = 0; mb < NMB; ++mb) {
+          oacc16[mb][0] *= a0;
+          oacc16[mb][1] *= a1;
         }
-    }
-    // Lazy rescale: move m only when a row's max outgrows it by > 2^8.
-    float mx[NQB];
-    bool grow = false;
+      } else {
 #pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
-      float t = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) t = fmaxf(t, s[kb][qb][r]);
-      mx[qb] = half_swap_max(t) * scale_log2;
-      grow |= mx[qb] > m_use[qb] + kRescaleSlack;
-    }
-    if (__builtin_amdgcn_ballot_w64(grow)) {
-#pragma unroll
-      for (int qb = 0; qb < NQB; ++qb) {
-        const float m_new = fmaxf(m_use[qb], mx[qb]);
-        const float alpha = __builtin_amdgcn_exp2f(m_use[qb] - m_new);  // 0 on the first tile
-        m_use[qb] = m_new;
-        l_run[qb] *= alpha;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) oacc[qb][db] *= alpha;
-      }
-    }
-    bf16x8 pb[2][2][NQB];
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
-      // every row has a finite max after its first tile (key 0 is visible)
-      const float mneg = -m_use[qb];
-      float lsum = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][qb][r], scale_log2, mneg));
-          s[kb][qb][r] = p;
-          if (!S::ONES_ROW) lsum += p;
-        }
-      if (!S::ONES_ROW) l_run[qb] += lsum;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) pb[kb][hh][qb][e] = __bf16(s[kb][qb][8 * hh + e]);
-    }
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          // keys 32kb + 16hh + 4g + {0..3} and + 8 + {0..3}; column 32db + (lane % 32)
-          const lds_bf16* p = Vs3 + vb0 + (32 * kb + 16 * hh) * VSTR + 32 * db;
-          const bf16x8 a = cat(lds_read_tr(p), lds_read_tr(p + 8 * VSTR));
-#pragma unroll
-          for (int qb = 0; qb < NQB; ++qb) oacc[qb][db] = mfma32(a, pb[kb][hh][qb], oacc[qb][db]);
-        }
+        for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
       }
     }
   };
 
-  // Each wavefront walks the key tiles in up to three phases: tiles that
-  // need no mask, the (at most two) tiles crossing the sequence end or its
-  // causal diagonal, and, when causal, tiles entirely above its queries.
-  // Every phase runs the same copy / wait / barrier sequence, so all
-  // wavefronts meet the same number of barriers.
-  const int n_full = seqlen / BN;  // tiles lying entirely inside the sequence
-  int t_mask = min(n_tiles, n_full);
-  int t_idle = n_tiles;
-  if (CAUSAL) {
-    t_mask = min(t_mask, (wave_q0 + 1) / BN);  // tiles whose last key is <= the wave's first query
-    t_idle = min(n_tiles, wave_last_q / BN + 1);
-  }
-  auto run = [&](int kt0, int kt1, auto mode_tag) {
-    constexpr int MODE = decltype(mode_tag)::value;  // 0 unmasked, 1 masked, 2 idle
-    for (int kt = kt0; kt < kt1; ++kt) {
-      const unsigned st = unsigned(kt) % 3;
-      if (kt + 2 < n_tiles) issue_tile(kt + 2);
-      if constexpr (MODE == 0) process_tile(st, kt * BN, std::false_type{});
-      if constexpr (MODE == 1) process_tile(st, kt * BN, std::true_type{});
-      wait_next(kt);
-      __syncthreads();
-    }
-  };
-  run(0, t_mask, std::integral_constant<int, 0>{});
-  run(t_mask, t_idle, std::integral_constant<int, 1>{});
-  if (CAUSAL) run(t_idle, n_tiles, std::integral_constant<int, 2>{});
-
-  // Epilogue.
+  // O^T += V^T P^T for the current block (V rows at vcur, this lane's
+  // transposing-read offset included).  32x32 blocks: A = V^T rows
+  // 32db + (lane % 32) over keys 16hh + 4g + {0..3, 8..11}, B = pb[hh]
+  // as it is.  16x16 blocks: two lane-row swaps turn pb into the B
+  // operands of queries 0..15 and 16..31, lane group g4 then holding keys
+  // {0..3, 8..11}, {16..19, 24..27}, {4..7, 12..15}, {20..23, 28..31} for
+  // g4 = 0..3, and the A operand of each 16-row block of V^T (two
+  // transposing reads of those key runs) feeds both query blocks.
+  auto pv_product = [&](const bf16x8 (&pb)[2], unsigned vcur) {
+    if constexpr (S::PV16) {
+      u32x4 x = __builtin_bit_cast(u32x4, pb[0]), y = __builtin_bit_cast(u32x4, pb[1]);
 #pragma unroll
-  for (int qb = 0; qb < NQB; ++qb) {
-    float l_tot;
-    if (S::ONES_ROW) {
-      // row D of O^T: block NDB-1, in-block row D - 32*(NDB-1), held by g = 0 lanes
-      constexpr int rr = D - 32 * (NDB - 1);
-      constexpr int reg = 4 * (rr / 8) + (rr % 4);
-      static_assert((rr % 8) < 4, "row-sum row must sit in the g = 0 half");
-      const float mine = oacc[qb][NDB - 1][reg];
-      auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mine), __float_as_uint(mine), false, false);
-      l_tot = __uint_as_float(sw[0]);  // lanes < 32 keep their own, lanes >= 32 get lane - 32
+      for (int i = 0; i < 4; ++i) {
+        auto sw = __builtin_amdgcn_permlane16_swap(x[i], y[i], false, false);
+        x[i] = sw[0];
+        y[i] = sw[1];
+      }
+      const bf16x8 b0 = __builtin_bit_cast(bf16x8, x), b1 = __builtin_bit_cast(bf16x8, y);
+#pragma unroll
+      for (int mb = 0; mb < NMB; ++mb) {
+        const lds_bf16* p = Vs3 + vcur + 16 * mb;
+        const bf16x8 a = cat(lds_read_tr(p), lds_read_tr(p + 8 * VSTR));
+        oacc16[mb][0] = mfma16(a, b0, oacc16[mb][0]);
+        oacc16[mb][1] = mfma16(a, b1, oacc16[mb][1]);
+      }
     } else {
-      l_tot = half_swap_sum(l_run[qb]);
-    }
-    const float inv = 1.f / l_tot;
-    const int qrel = wave * QPW + 32 * qb + j;
-    if (qrel < u.rows) {
-      const int64_t row = int64_t(u.row0) + qrel;
-      __bf16* orow = o + row * ts + int64_t(h) * D;
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
-          const int d0 = 32 * db + 8 * rb + 4 * g;
+        for (int hh = 0; hh < 2; ++hh) {
+          const lds_bf16* p = Vs3 + vcur + 16 * hh * VSTR + 32 * db;
+          oacc[db] = mfma32(cat(lds_read_tr(p), lds_read_tr(p + 8 * VSTR)), pb[hh], oacc[db]);
+        }
+    }
+  };
+
+#pragma unroll
+  for (int t = 0; t < PD; ++t)
+    if (t < n_tiles) issue_tile(t);
+  wait_for(0);
+  __syncthreads();
+
+  f32x16 sc{};  // S^T of the current block, masked, not yet exponentiated
+  if (nb > 0) {
+    unsigned kb0 = kr_off;
+    asm("" : "+v"(kb0));
+    sc = scores(kb0);
+    if (b_mask == 0) apply_mask(sc, 0);
+    rescale(row_max(sc), true);
+  }
+
+  // One pipelined step: P and O for the current block (V rows at vcur)
+  // while the scores of block bn (K rows at knext) are computed, masked
+  // when MASK, and their row max taken.  On a wavefront's last block the
+  // successor's scores are computed but not used (valid_next false).
+  auto step = [&](int bn, unsigned knext, unsigned vcur, bool valid_next, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    f32x16 sn = scores(knext);
+    // P = exp2(S*scale*log2e - m) as bf16 (B operand of the PV product)
+    const float mneg = -m_use;
+    bf16x8 pb[2];
+    float lsum = 0.f;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sc[8 * hh + e], scale_log2, mneg));
+        if (!S::ONES_ROW) lsum += p;
+        pb[hh][e] = __bf16(p);
+      }
+    if (!S::ONES_ROW) l_run += lsum;
+    if constexpr (MASK) apply_mask(sn, bn);
+    pv_product(pb, vcur);
+    if (DCP_FWD_SCHED) {
+      // every LDS read first, then the S products of the next block between
+      // the exponentials, then the PV products between the row-max steps
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, NKD + 4 * NDB, 0);
+#pragma unroll
+      for (int i = 0; i < NKD; ++i) {
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedValu, 40 / NKD, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 2 * NDB; ++i) {
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedValu, 2, 0);
+      }
+    }
+    rescale(row_max(sn), valid_next);
+    sc = sn;
+  };
+
+  // Tile kt: blocks 2kt and 2kt + 1; the successor of the second block is
+  // the first block of tile kt + 1.
+  auto tile = [&](int kt, auto mask_tag) {
+    if (kt + PD < n_tiles) issue_tile(kt + PD);
+    unsigned kb0 = (unsigned(kt) % NST) * KBUF + kr_off;
+    unsigned kb1 = (unsigned(kt + 1) % NST) * KBUF + kr_off;
+    unsigned vb0 = (unsigned(kt) % NST) * VBUF + tr_lane;
+    asm("" : "+v"(kb0), "+v"(kb1), "+v"(vb0));  // keeps the constant terms in the offset fields
+    step(2 * kt + 1, kb0 + 32 * KSTR, vb0, 2 * kt + 1 < 2 * t_work, mask_tag);
+    step(2 * kt + 2, kb1, vb0 + 32 * VSTR, 2 * kt + 2 < 2 * t_work, mask_tag);
+    wait_for(kt + 1);
+    __syncthreads();
+  };
+  int kt = 0;
+  for (; kt < t_plain; ++kt) tile(kt, std::false_type{});
+  for (; kt < t_work; ++kt) tile(kt, std::true_type{});
+  for (; kt < n_tiles; ++kt) {
+    if (kt + PD < n_tiles) issue_tile(kt + PD);
+    wait_for(kt + 1);
+    __syncthreads();
+  }
+
+  // Epilogue.
+  if constexpr (S::PV16) {
+    // the row-sum row D sits in block NMB-1, row D % 16: lane group
+    // (D % 16) / 4, register D % 4, of the lanes holding queries n, 16 + n
+    constexpr int rg = (D % 16) / 4, rr = D % 4;
+    const int src = 16 * rg + (lane & 15);
+    const float l0 = __shfl(oacc16[NMB - 1][0][rr], src);
+    const float l1 = __shfl(oacc16[NMB - 1][1][rr], src);
+    const float inv[2] = {1.f / l0, 1.f / l1};
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int qrel = wave * 32 + 16 * qb + (lane & 15);
+      if (qrel < u.rows) {
+        __bf16* orow = o + (int64_t(u.row0) + qrel) * ts + int64_t(h) * D;
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) {
+          const int d0 = 16 * mb + 4 * g4;
           if (d0 < D) {
             bf16x4 w;
 #pragma unroll
-            for (int c = 0; c < 4; ++c) w[c] = __bf16(oacc[qb][db][4 * rb + c] * inv);
+            for (int c = 0; c < 4; ++c) w[c] = __bf16(oacc16[mb][qb][c] * inv[qb]);
             *reinterpret_cast<bf16x4*>(orow + d0) = w;
           }
         }
-      if (g == 0) lse[int64_t(h) * T + row] = (m_use[qb] + __log2f(l_tot)) * kLn2;
+      }
     }
+    const int qrel = wave * 32 + j;
+    if (g == 0 && qrel < u.rows)
+      lse[int64_t(h) * T + u.row0 + qrel] = (m_use + __log2f((j & 16) ? l1 : l0)) * kLn2;
+    return;
+  }
+  float l_tot;
+  if (S::ONES_ROW) {
+    // row D of O^T: block NDB-1, in-block row D - 32*(NDB-1), held by g = 0 lanes
+    constexpr int rr = D - 32 * (NDB - 1);
+    constexpr int reg = 4 * (rr / 8) + (rr % 4);
+    static_assert((rr % 8) < 4, "row-sum row must sit in the g = 0 half");
+    const float mine = oacc[NDB - 1][reg];
+    auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mine), __float_as_uint(mine), false, false);
+    l_tot = __uint_as_float(sw[0]);  // lanes < 32 keep their own, lanes >= 32 get lane - 32
+  } else {
+    l_tot = half_swap_sum(l_run);
+  }
+  const float inv = 1.f / l_tot;
+  const int qrel = wave * 32 + j;
+  if (qrel < u.rows) {
+    const int64_t row = int64_t(u.row0) + qrel;
+    __bf16* orow = o + row * ts + int64_t(h) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        const int d0 = 32 * db + 8 * rb + 4 * g;
+        if (d0 < D) {
+          bf16x4 w;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) w[c] = __bf16(oacc[db][4 * rb + c] * inv);
+          *reinterpret_cast<bf16x4*>(orow + d0) = w;
+        }
+      }
+    if (g == 0) lse[int64_t(h) * T + row] = (m_use + __log2f(l_tot)) * kLn2;
   }
 }
 
-template <int D, int NQB, int NW, bool CAUSAL>
+template <int D, int NW, bool CAUSAL>
 hipError_t launch_fwd_t(const FwdArgs& a) {
   dim3 grid(a.n_units);
   const KernelEvents& ev = kernel_events();
   if (ev.begin) (void)hipEventRecord(ev.begin, a.stream);
-  hipLaunchKernelGGL((attn_fwd_kernel<D, NQB, NW, CAUSAL>), grid, dim3(64 * NW), 0, a.stream,
+  hipLaunchKernelGGL((attn_fwd_kernel<D, NW, CAUSAL>), grid, dim3(64 * NW), 0, a.stream,
                      static_cast<const __bf16*>(a.q), static_cast<const __bf16*>(a.k),
                      static_cast<const __bf16*>(a.v), static_cast<__bf16*>(a.o), a.lse,
                      static_cast<const __bf16*>(a.consts), static_cast<const WorkUnit*>(a.units),
@@ -336,15 +435,15 @@ hipError_t launch_fwd_t(const FwdArgs& a) {
 
 }  // namespace
 
-int fwd_tile_rows(int head_dim) { return kFwdWaves * 32 * kFwdNQB; }
+int fwd_tile_rows(int head_dim) { return kFwdWaves * 32; }
 
 hipError_t launch_fwd(const FwdArgs& a) {
   if (a.n_units == 0) return hipSuccess;
-  constexpr int Q = kFwdNQB, W = kFwdWaves;
+  constexpr int W = kFwdWaves;
   switch (a.head_dim) {
-    case 64: return a.causal ? launch_fwd_t<64, Q, W, true>(a) : launch_fwd_t<64, Q, W, false>(a);
-    case 72: return a.causal ? launch_fwd_t<72, Q, W, true>(a) : launch_fwd_t<72, Q, W, false>(a);
-    case 128: return a.causal ? launch_fwd_t<128, Q, W, true>(a) : launch_fwd_t<128, Q, W, false>(a);
+    case 64: return a.causal ? launch_fwd_t<64, W, true>(a) : launch_fwd_t<64, W, false>(a);
+    case 72: return a.causal ? launch_fwd_t<72, W, true>(a) : launch_fwd_t<72, W, false>(a);
+    case 128: return a.causal ? launch_fwd_t<128, W, true>(a) : launch_fwd_t<128, W, false>(a);
     default: return hipErrorInvalidValue;
   }
 }

@@ -6,14 +6,10 @@
 
 namespace dcp {
 
-// Query rows per forward workgroup: kFwdWaves wavefronts x 32 x kFwdNQB.
-#ifndef DCP_FWD_NQB
-#define DCP_FWD_NQB 1
-#endif
+// Query rows per forward workgroup: kFwdWaves wavefronts x 32.
 #ifndef DCP_FWD_WAVES
 #define DCP_FWD_WAVES 8
 #endif
-constexpr int kFwdNQB = DCP_FWD_NQB;
 constexpr int kFwdWaves = DCP_FWD_WAVES;
 // Backward, dK/dV pass: `waves` wavefronts per workgroup, each owning
 // 32*kb keys whose K, V fragments and dK, dV accumulators stay resident,
