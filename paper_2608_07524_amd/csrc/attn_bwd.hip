@@ -51,6 +51,10 @@ struct BwdShape {
   static constexpr int W = (DP > NDB * 32) ? DP : NDB * 32;
   static constexpr int RSTR = W + 8;                                  // both ways
   static constexpr int TSTR = (NDB * 32 % 64 == 32) ? NDB * 32 : NDB * 32 + 32;  // transposing only
+  // dK and dV from 16x16x32 products when 16-column blocks cover D with
+  // fewer padded columns than 32-column blocks (D = 72: 80 instead of 96).
+  static constexpr int NMB = (D + 15) / 16;
+  static constexpr bool KV16 = NMB * 16 < NDB * 32;
 };
 
 // ---------------------------------------------------------------------------
@@ -117,6 +121,51 @@ __device__ __forceinline__ void store_rows_bf16(const f32x16 (&acc)[NDB], float 
           *reinterpret_cast<const u32x4*>(&stage[row * st + cc * 8]);
   }
   wave_lds_sync();
+}
+
+// The same for accumulators in 16x16 blocks [key block][column block]
+// (C layout of v_mfma_f32_16x16x32: lane (g4, n) holds column 16*nb + n of
+// rows 16*mb + 4*g4 + r).
+template <int D, int NMB>
+__device__ __forceinline__ void store_rows16_bf16(const f32x4 (&acc)[2][NMB], float mul, __bf16* stage, int st,
+                                                  __bf16* __restrict__ base, int64_t row_stride, int n_rows,
+                                                  int lane) {
+  const int g4 = lane >> 4, n = lane & 15;
+  wave_lds_sync();
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NMB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) stage[(16 * mb + 4 * g4 + r) * st + 16 * nb + n] = __bf16(acc[mb][nb][r] * mul);
+  wave_lds_sync();
+  constexpr int CPR = D / 8;
+  for (int ch = lane; ch < 32 * CPR; ch += 64) {
+    const int row = ch / CPR, cc = ch % CPR;
+    if (row < n_rows)
+      *reinterpret_cast<u32x4*>(base + int64_t(row) * row_stride + cc * 8) =
+          *reinterpret_cast<const u32x4*>(&stage[row * st + cc * 8]);
+  }
+  wave_lds_sync();
+}
+
+// Moves the two halves of a 32x32 accumulator-layout operand (lane (g, j):
+// index j, contraction values {8b + 4g + c}, b in {0,1} in x and {2,3} in
+// y) into the 16x16x32 layout: x becomes the operand of indices 0..15 and
+// y that of indices 16..31, lane group g4 = lane / 16 then holding the
+// contraction values {0..3, 8..11}, {16..19, 24..27}, {4..7, 12..15},
+// {20..23, 28..31} for g4 = 0..3 (v_permlane16_swap exchanges the odd
+// 16-lane rows of x with the even rows of y).
+__device__ __forceinline__ void to_mfma16_layout(bf16x8& xv, bf16x8& yv) {
+  u32x4 x = __builtin_bit_cast(u32x4, xv), y = __builtin_bit_cast(u32x4, yv);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    auto sw = __builtin_amdgcn_permlane16_swap(x[i], y[i], false, false);
+    x[i] = sw[0];
+    y[i] = sw[1];
+  }
+  xv = __builtin_bit_cast(bf16x8, x);
+  yv = __builtin_bit_cast(bf16x8, y);
 }
 
 // ---------------------------------------------------------------------------
@@ -237,6 +286,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
       dk_acc[kb][db] = f32x16{};
       dv_acc[kb][db] = f32x16{};
     }
+  // KV16: [key block][16-key half][16-column block]
+  constexpr int NMB = S::NMB;
+  f32x4 dk16[KB][2][NMB], dv16[KB][2][NMB];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NMB; ++nb) dk16[kb][mb][nb] = dv16[kb][mb][nb] = f32x4{};
 
   issue_tile(0);
   if (NSTAGE == 3 && n_qt > 1) issue_tile(1);
@@ -247,7 +305,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   // operands) and transposing reads (see lds_read_tr); every other term is
   // a compile-time constant.
   const unsigned ar_off = j * RSTR + 8 * g;
-  const unsigned tr_off = (4 * g + ((lane & 15) >> 2)) * TSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  // (KV16: lane group g4 reads the query runs starting at 0, 16, 4, 20
+  // and 8 further, matching to_mfma16_layout)
+  const int g4 = lane >> 4;
+  const unsigned tr_off =
+      S::KV16 ? (16 * (g4 & 1) + 4 * (g4 >> 1) + ((lane & 15) >> 2)) * TSTR + 4 * (lane & 3)
+              : (4 * g + ((lane & 15) >> 2)) * TSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const lds_bf16* Qr3 = lds_ptr(Qr);
   const lds_bf16* dOr3 = lds_ptr(dOr);
   const lds_bf16* Qt3 = lds_ptr(Qt);
@@ -309,6 +372,32 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
           pa[kb][b >> 1][4 * (b & 1) + c] = __bf16(p);
           da[kb][b >> 1][4 * (b & 1) + c] = __bf16(p * dp[kb][r]);
         }
+    }
+    if constexpr (S::KV16) {
+      // dV += P^T dO and dK += dS^T Q in 16x16 blocks: each B fragment (16
+      // columns of dO or Q over the block's 32 queries) feeds both 16-key
+      // halves.
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        to_mfma16_layout(pa[kb][0], pa[kb][1]);
+        to_mfma16_layout(da[kb][0], da[kb][1]);
+      }
+      mfma_prio_hi();
+#pragma unroll
+      for (int nb = 0; nb < NMB; ++nb) {
+        const unsigned o = tb + 16 * nb;
+        const bf16x8 bd = cat(lds_read_tr(dOt3 + o), lds_read_tr(dOt3 + o + 8 * TSTR));
+        const bf16x8 bqq = cat(lds_read_tr(Qt3 + o), lds_read_tr(Qt3 + o + 8 * TSTR));
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+          for (int mb = 0; mb < 2; ++mb) {
+            dv16[kb][mb][nb] = mfma16(pa[kb][mb], bd, dv16[kb][mb][nb]);
+            dk16[kb][mb][nb] = mfma16(da[kb][mb], bqq, dk16[kb][mb][nb]);
+          }
+      }
+      mfma_prio_lo();
+      return;
     }
     // dV += P^T dO and dK += dS^T Q: B = rows (queries) x columns (d),
     // fetched column-wise with transposing reads, shared by the key blocks.
@@ -380,8 +469,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
     const int n_rows = max(0, min(32, u.rows - key0));
     __bf16* dk_base = dk + int64_t(u.row0 + key0) * ts + int64_t(h) * D;
     __bf16* dv_base = dv + int64_t(u.row0 + key0) * ts + int64_t(h) * D;
-    store_rows_bf16<D, NDB>(dk_acc[kb], scale, stage, SSTR, dk_base, ts, n_rows, lane);
-    store_rows_bf16<D, NDB>(dv_acc[kb], 1.f, stage, SSTR, dv_base, ts, n_rows, lane);
+    if constexpr (S::KV16) {
+      store_rows16_bf16<D, NMB>(dk16[kb], scale, stage, SSTR, dk_base, ts, n_rows, lane);
+      store_rows16_bf16<D, NMB>(dv16[kb], 1.f, stage, SSTR, dv_base, ts, n_rows, lane);
+    } else {
+      store_rows_bf16<D, NDB>(dk_acc[kb], scale, stage, SSTR, dk_base, ts, n_rows, lane);
+      store_rows_bf16<D, NDB>(dv_acc[kb], 1.f, stage, SSTR, dv_base, ts, n_rows, lane);
+    }
   }
 }
 
