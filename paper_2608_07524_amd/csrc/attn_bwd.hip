@@ -578,6 +578,12 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   f32x16 acc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
+  // KV16: dQ^T in 16x16 blocks [d block][query block]; lane (g4, n) holds
+  // query 16 * qb + n, columns 16 * mb + 4 * g4 + {0..3}
+  constexpr int NMB = S::NMB;
+  f32x4 acc16[NMB][2];
+#pragma unroll
+  for (int mb = 0; mb < NMB; ++mb) acc16[mb][0] = acc16[mb][1] = f32x4{};
 
   if (n_tiles > 0) issue_tile(0);
   if (NSTAGE == 3 && n_tiles > 1) issue_tile(1);
@@ -585,7 +591,12 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   __syncthreads();
 
   const unsigned ar_off = j * KSTR + 8 * g;
-  const unsigned tr_off = (4 * g + ((lane & 15) >> 2)) * TSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  // (KV16: lane group g4 reads the key runs starting at 0, 16, 4, 20 and 8
+  // further, matching to_mfma16_layout)
+  const int g4 = lane >> 4;
+  const unsigned tr_off =
+      S::KV16 ? (16 * (g4 & 1) + 4 * (g4 >> 1) + ((lane & 15) >> 2)) * TSTR + 4 * (lane & 3)
+              : (4 * g + ((lane & 15) >> 2)) * TSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const lds_bf16* Ks3 = lds_ptr(Ks);
   const lds_bf16* Vs3 = lds_ptr(Vs);
   const lds_bf16* Kt3 = lds_ptr(Kt);
@@ -629,6 +640,24 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
         }
         dsb[kb][r >> 3][r & 7] = __bf16(p * (FOLD ? dp[kb][r] : dp[kb][r] + ndlt));
       }
+    if constexpr (S::KV16) {
+      // dQ^T += K^T dS^T in 16x16 blocks: each A fragment (16 rows of K^T
+      // over the block's 32 keys) feeds both 16-query halves.
+#pragma unroll
+      for (int kb = 0; kb < BN / 32; ++kb) to_mfma16_layout(dsb[kb][0], dsb[kb][1]);
+      mfma_prio_hi();
+#pragma unroll
+      for (int kb = 0; kb < BN / 32; ++kb)
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) {
+          const unsigned o = tb + 32 * kb * TSTR + 16 * mb;
+          const bf16x8 a = cat(lds_read_tr(Kt3 + o), lds_read_tr(Kt3 + o + 8 * TSTR));
+          acc16[mb][0] = mfma16(a, dsb[kb][0], acc16[mb][0]);
+          acc16[mb][1] = mfma16(a, dsb[kb][1], acc16[mb][1]);
+        }
+      mfma_prio_lo();
+      return;
+    }
     // dQ^T += K^T dS^T: A = K^T (rows d, keys 32kb + 16hh + 4g + {0..3, 8..11}).
     mfma_prio_hi();
 #pragma unroll
@@ -667,6 +696,26 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   run(t_mask, t_idle, std::integral_constant<int, 1>{});
   if (CAUSAL) run(t_idle, n_tiles, std::integral_constant<int, 2>{});
 
+  if constexpr (S::KV16) {
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int qr = 32 * wave + 16 * qb + (lane & 15);
+      if (qr < u.rows) {
+        __bf16* qrow = dq + int64_t(u.row0 + qr) * ts + int64_t(h) * D;
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) {
+          const int d0 = 16 * mb + 4 * g4;
+          if (d0 < D) {
+            bf16x4 w;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) w[c] = __bf16(acc16[mb][qb][c] * scale);
+            *reinterpret_cast<bf16x4*>(qrow + d0) = w;
+          }
+        }
+      }
+    }
+    return;
+  }
   // Epilogue: lane (g, j) holds query j, columns 32db + 8rb + 4g + {0..3}.
   if (q_ok) {
     __bf16* qrow = dq + int64_t(u.seq0 + my_q) * ts + int64_t(h) * D;
