@@ -257,16 +257,29 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   const int q_begin = CAUSAL ? (key_t0 / BM) * BM : 0;
   const int n_qt = (seqlen - q_begin + BM - 1) / BM;
 
+  // Full query tiles take the scalar-base copies, except in the causal
+  // one-wavefront-per-SIMD variant: its resident state leaves no registers
+  // for the precomputed offsets (holding them pushes values into scratch).
+  constexpr bool kFullCopies = !(CAUSAL && WPE == 1);
+  const typename DR::FullOffsets fo_r = DR::full_offsets(ts, wave, lane);
+  const typename DT::FullOffsets fo_t = DT::full_offsets(ts, wave, lane);
   auto issue_tile = [&](int it) {
     const unsigned st = unsigned(it) % NSTAGE;
     const int q0 = q_begin + it * BM;
     const int valid = seqlen - q0;
     const __bf16* qs = qh + int64_t(q0) * ts;
     const __bf16* ds = doh + int64_t(q0) * ts;
-    DR::issue(&Qr[st * RBUF], qs, ts, valid, zero, zero, wave, lane);
-    DT::issue(&Qt[st * TBUF], qs, ts, valid, zero, zero, wave, lane);
-    DR::issue(&dOr[st * RBUF], ds, ts, valid, zero, zero, wave, lane);
-    DT::issue(&dOt[st * TBUF], ds, ts, valid, zero, zero, wave, lane);
+    if (kFullCopies && valid >= BM) {
+      DR::issue_full(&Qr[st * RBUF], qs, fo_r, wave);
+      DT::issue_full(&Qt[st * TBUF], qs, fo_t, wave);
+      DR::issue_full(&dOr[st * RBUF], ds, fo_r, wave);
+      DT::issue_full(&dOt[st * TBUF], ds, fo_t, wave);
+    } else {
+      DR::issue(&Qr[st * RBUF], qs, ts, valid, zero, zero, wave, lane);
+      DT::issue(&Qt[st * TBUF], qs, ts, valid, zero, zero, wave, lane);
+      DR::issue(&dOr[st * RBUF], ds, ts, valid, zero, zero, wave, lane);
+      DT::issue(&dOt[st * TBUF], ds, ts, valid, zero, zero, wave, lane);
+    }
     // A query past the sequence end gets LSE = +inf, so its P is exactly 0.
     DL::issue(&LV[st * 2 * BM], lseh + q0, ndh + q0, valid, finf, fzero, wave, lane);
   };
@@ -557,13 +570,21 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   const int key_end = CAUSAL ? min(seqlen, tile_q0 + u.rows) : seqlen;
   const int n_tiles = (key_end + BN - 1) / BN;
 
+  const typename DK::FullOffsets fo_k = DK::full_offsets(ts, wave, lane);
+  const typename DT::FullOffsets fo_t = DT::full_offsets(ts, wave, lane);
   auto issue_tile = [&](int kt) {
     const unsigned st = unsigned(kt) % NSTAGE;
     const int valid = seqlen - kt * BN;
     const __bf16* ks = kh + int64_t(kt) * BN * ts;
-    DK::issue(&Ks[st * KBUF], ks, ts, valid, zero, zero, wave, lane);
-    DK::issue(&Vs[st * KBUF], vh + int64_t(kt) * BN * ts, ts, valid, zero, zero, wave, lane);
-    DT::issue(&Kt[st * TBUF], ks, ts, valid, zero, zero, wave, lane);
+    if (valid >= BN) {
+      DK::issue_full(&Ks[st * KBUF], ks, fo_k, wave);
+      DK::issue_full(&Vs[st * KBUF], vh + int64_t(kt) * BN * ts, fo_k, wave);
+      DT::issue_full(&Kt[st * TBUF], ks, fo_t, wave);
+    } else {
+      DK::issue(&Ks[st * KBUF], ks, ts, valid, zero, zero, wave, lane);
+      DK::issue(&Vs[st * KBUF], vh + int64_t(kt) * BN * ts, ts, valid, zero, zero, wave, lane);
+      DT::issue(&Kt[st * TBUF], ks, ts, valid, zero, zero, wave, lane);
+    }
   };
   // Before the barrier that ends tile kt: tile kt+1 must have landed; only
   // tile kt+2's copies (three stages: issued this iteration) may still be

@@ -165,6 +165,50 @@ struct DmaTile {
     }
   }
 
+  // Full tiles (every row inside the sequence): this lane's byte offsets
+  // from the tile's first row, one per copy it issues.  Slot (r, c) reads
+  // chunk c of row r when c < CPR_DATA and chunk 0 of the same row
+  // otherwise (such columns are either multiplied by zero register
+  // operands or produce output columns that are never stored); slots past
+  // the tile repeat its last row.  The offsets do not change from tile to
+  // tile, so a full tile's copies take no vector arithmetic.
+  struct FullOffsets {
+    uint32_t off[NI];
+  };
+  __device__ __forceinline__ static FullOffsets full_offsets(int64_t row_stride, int wave, int lane) {
+    FullOffsets fo;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int t = min(wave + NW * i, NINS - 1);
+      const int slot = 64 * t + lane;
+      const int r = min(slot / CPR_PAD, ROWS - 1), c = slot % CPR_PAD;
+      fo.off[i] = uint32_t((int64_t(r) * row_stride + 8 * (c < CPR_DATA ? c : 0)) * 2);
+    }
+    return fo;
+  }
+  // Copies a full tile whose first row is at `src` (wavefront-uniform):
+  // scalar base plus the precomputed offsets (global_load_lds_dwordx4 in
+  // its scalar-base form).
+  __device__ __forceinline__ static void issue_full(__bf16* lds_tile, const __bf16* src, const FullOffsets& fo,
+                                                    int wave) {
+    // (readfirstlane returns a signed int: both halves go through uint32_t
+    // so the low word is zero-extended, never sign-extended into the high one)
+    const uint64_t a = reinterpret_cast<uint64_t>(src);
+    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32)));
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a)));
+    const uint64_t base = (uint64_t(hi) << 32) | uint64_t(lo);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int t = min(wave + NW * i, NINS - 1);
+      const uint32_t m0 = __builtin_amdgcn_readfirstlane(
+          static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds_tile + 512 * t)));
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                   :
+                   : "s"(m0), "v"(fo.off[i]), "s"(base)
+                   : "memory");
+    }
+  }
+
   // One global_load_lds_dwordx4: lane i's 16 bytes at `g` land in LDS at
   // `lds_base` + 16*i.  Written as inline assembly: the compiler would
   // otherwise treat the copy as possibly aliasing every LDS read and wait

@@ -151,11 +151,23 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   const int t_work = (nb + 1) / 2;
   const int t_plain = b_mask >= 1 ? (b_mask - 1) / 2 : 0;  // tiles kt with 2kt + 2 < b_mask
 
+  // (full K tiles take the scalar-base copies; V keeps per-lane addresses
+  // when its first pad column must hold the ones of the row-sum row)
+  const typename DK::FullOffsets fo_k = DK::full_offsets(ts, wave, lane);
+  const typename DV::FullOffsets fo_v = DV::full_offsets(ts, wave, lane);
   auto issue_tile = [&](int kt) {
     const unsigned st = unsigned(kt) % NST;
     const int valid = min(BN, seqlen - kt * BN);
-    DK::issue(&Ks[st * KBUF], kh + int64_t(kt) * BN * ts, ts, valid, zero, zero, wave, lane);
-    DV::issue(&Vs[st * VBUF], vh + int64_t(kt) * BN * ts, ts, valid, zero, v_pad, wave, lane);
+    if (valid == BN) {
+      DK::issue_full(&Ks[st * KBUF], kh + int64_t(kt) * BN * ts, fo_k, wave);
+    } else {
+      DK::issue(&Ks[st * KBUF], kh + int64_t(kt) * BN * ts, ts, valid, zero, zero, wave, lane);
+    }
+    if (valid == BN && !S::ONES_ROW) {
+      DV::issue_full(&Vs[st * VBUF], vh + int64_t(kt) * BN * ts, fo_v, wave);
+    } else {
+      DV::issue(&Vs[st * VBUF], vh + int64_t(kt) * BN * ts, ts, valid, zero, v_pad, wave, lane);
+    }
   };
   // Before tile kt is consumed, tiles kt and kt + 1 must have landed (the
   // scores of tile kt + 1's first block are computed while tile kt is
