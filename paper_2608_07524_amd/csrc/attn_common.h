@@ -209,6 +209,48 @@ struct DmaTile {
     }
   }
 
+  // As issue_full, but slot column SKIP of every row is left untouched
+  // (its lanes are masked off), so a constant written there once stays.
+  template <int SKIP>
+  struct SkipMasks {
+    uint64_t m[NI];
+  };
+  template <int SKIP>
+  __device__ __forceinline__ static SkipMasks<SKIP> skip_masks(int wave, int lane) {
+    SkipMasks<SKIP> sm;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int t = min(wave + NW * i, NINS - 1);
+      const int slot = 64 * t + lane;
+      sm.m[i] = __builtin_amdgcn_ballot_w64(slot % CPR_PAD != SKIP || slot / CPR_PAD >= ROWS);
+    }
+    return sm;
+  }
+  template <int SKIP>
+  __device__ __forceinline__ static void issue_full_skip(__bf16* lds_tile, const __bf16* src, const FullOffsets& fo,
+                                                         const SkipMasks<SKIP>& sm, int wave) {
+    const uint64_t a = reinterpret_cast<uint64_t>(src);
+    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32)));
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a)));
+    const uint64_t base = (uint64_t(hi) << 32) | uint64_t(lo);
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int t = min(wave + NW * i, NINS - 1);
+      const uint32_t m0 = __builtin_amdgcn_readfirstlane(
+          static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds_tile + 512 * t)));
+      uint64_t saved;
+      asm volatile(
+          "s_mov_b64 %0, exec\n\t"
+          "s_mov_b64 exec, %1\n\t"
+          "s_mov_b32 m0, %2\n\t"
+          "global_load_lds_dwordx4 %3, %4\n\t"
+          "s_mov_b64 exec, %0"
+          : "=&s"(saved)
+          : "s"(sm.m[i]), "s"(m0), "v"(fo.off[i]), "s"(base)
+          : "memory");
+    }
+  }
+
   // One global_load_lds_dwordx4: lane i's 16 bytes at `g` land in LDS at
   // `lds_base` + 16*i.  Written as inline assembly: the compiler would
   // otherwise treat the copy as possibly aliasing every LDS read and wait

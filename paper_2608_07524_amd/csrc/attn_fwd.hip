@@ -151,21 +151,32 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   const int t_work = (nb + 1) / 2;
   const int t_plain = b_mask >= 1 ? (b_mask - 1) / 2 : 0;  // tiles kt with 2kt + 2 < b_mask
 
-  // (full K tiles take the scalar-base copies; V keeps per-lane addresses
-  // when its first pad column must hold the ones of the row-sum row)
+  // Full tiles take the scalar-base copies.  When V's first pad column
+  // carries the ones of the row-sum row, that column is written once per
+  // ring stage here and full-tile copies leave it alone (partial tiles
+  // rewrite it with the same ones).
   const typename DK::FullOffsets fo_k = DK::full_offsets(ts, wave, lane);
   const typename DV::FullOffsets fo_v = DV::full_offsets(ts, wave, lane);
+  const auto vskip = DV::template skip_masks<CPR>(wave, lane);
+  if constexpr (S::ONES_ROW) {
+    for (int idx = tid; idx < NST * BN; idx += 64 * NW) {
+      const int st = idx / BN, r = idx % BN;
+      *reinterpret_cast<bf16x8*>(&Vs[st * VBUF + r * VSTR + 8 * CPR]) =
+          bf16x8{__bf16(1.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f)};
+    }
+  }
   auto issue_tile = [&](int kt) {
     const unsigned st = unsigned(kt) % NST;
     const int valid = min(BN, seqlen - kt * BN);
     if (valid == BN) {
       DK::issue_full(&Ks[st * KBUF], kh + int64_t(kt) * BN * ts, fo_k, wave);
+      if constexpr (S::ONES_ROW) {
+        DV::issue_full_skip(&Vs[st * VBUF], vh + int64_t(kt) * BN * ts, fo_v, vskip, wave);
+      } else {
+        DV::issue_full(&Vs[st * VBUF], vh + int64_t(kt) * BN * ts, fo_v, wave);
+      }
     } else {
       DK::issue(&Ks[st * KBUF], kh + int64_t(kt) * BN * ts, ts, valid, zero, zero, wave, lane);
-    }
-    if (valid == BN && !S::ONES_ROW) {
-      DV::issue_full(&Vs[st * VBUF], vh + int64_t(kt) * BN * ts, fo_v, wave);
-    } else {
       DV::issue(&Vs[st * VBUF], vh + int64_t(kt) * BN * ts, ts, valid, zero, v_pad, wave, lane);
     }
   };
