@@ -463,13 +463,22 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
       __syncthreads();
     }
   };
-  int it_plain = 0;
-  if (CAUSAL) {
-    // first tile whose queries all follow all of this wavefront's keys
-    it_plain = min(n_qt, max(0, (wave_key_lo + 32 * KB - 1 - q_begin + BM - 1) / BM));
-    run(0, it_plain, std::true_type{});
+  if (32 * KB * wave < u.rows) {
+    int it_plain = 0;
+    if (CAUSAL) {
+      // first tile whose queries all follow all of this wavefront's keys
+      it_plain = min(n_qt, max(0, (wave_key_lo + 32 * KB - 1 - q_begin + BM - 1) / BM));
+      run(0, it_plain, std::true_type{});
+    }
+    run(it_plain, n_qt, std::false_type{});
+  } else {
+    // no key of the tile (the last tile of a sequence): copies and barriers only
+    for (int it = 0; it < n_qt; ++it) {
+      if (it + NSTAGE - 1 < n_qt) issue_tile(it + NSTAGE - 1);
+      wait_next(it);
+      __syncthreads();
+    }
   }
-  run(it_plain, n_qt, std::false_type{});
 
   // Epilogue through LDS (the ring is idle now): the workgroup's first half
   // of 32-key blocks is staged in the Q buffers, the second in the dO
@@ -695,13 +704,15 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   };
 
   // Key tiles in up to three phases per wavefront (unmasked, masked, idle),
-  // each with the same copy / wait / barrier sequence.
+  // each with the same copy / wait / barrier sequence.  A wavefront holding
+  // no query of the tile (the last tile of a sequence) only idles.
   int t_mask = min(n_tiles, seqlen / BN);
   int t_idle = n_tiles;
   if (CAUSAL) {
     t_mask = min(t_mask, (wave_q0 + 1) / BN);
     t_idle = min(n_tiles, wave_last_q / BN + 1);
   }
+  if (32 * wave >= u.rows) t_mask = t_idle = 0;
   auto run = [&](int kt0, int kt1, auto mode_tag) {
     constexpr int MODE = decltype(mode_tag)::value;  // 0 unmasked, 1 masked, 2 idle
     for (int kt = kt0; kt < kt1; ++kt) {
@@ -715,7 +726,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   };
   run(0, t_mask, std::integral_constant<int, 0>{});
   run(t_mask, t_idle, std::integral_constant<int, 1>{});
-  if (CAUSAL) run(t_idle, n_tiles, std::integral_constant<int, 2>{});
+  run(t_idle, n_tiles, std::integral_constant<int, 2>{});
 
   if constexpr (S::KV16) {
 #pragma unroll

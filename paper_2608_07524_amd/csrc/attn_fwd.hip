@@ -144,9 +144,10 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   // up to t_work tiles with masking on (a block past the wavefront's keys is
   // simply fully masked), then idles to n_tiles so that every wavefront
   // meets the same barriers.  A wavefront holding no query of the tile
-  // computes on zero queries; its rows are never stored.
+  // (the last tile of a sequence) only copies and idles.
+  const bool live = wave * 32 < u.rows;
   const int wave_keys = CAUSAL ? min(seqlen, wave_q0 + 32) : seqlen;
-  const int nb = min((wave_keys + 31) / 32, 2 * n_tiles);
+  const int nb = live ? min((wave_keys + 31) / 32, 2 * n_tiles) : 0;
   const int b_mask = min(nb, CAUSAL ? min(seqlen / 32, (wave_q0 + 1) / 32) : seqlen / 32);
   const int t_work = (nb + 1) / 2;
   const int t_plain = b_mask >= 1 ? (b_mask - 1) / 2 : 0;  // tiles kt with 2kt + 2 < b_mask
