@@ -72,6 +72,8 @@ def workload(name: str, seed: int = 0):
         return I.ulysses_shard(262144), rng
     if name == "text":
         return I.text_packs(rng, 1)[0], rng
+    if name in ("video2d_spatial", "video2d_temporal"):
+        return I.video_2d_pack(rng, name.split("_")[1]), rng
     raise SystemExit(f"unknown workload {name}")
 
 

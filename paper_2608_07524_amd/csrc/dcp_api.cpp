@@ -111,15 +111,19 @@ size_t tiles_per_head(const dcp_attn_desc* d, int tile) {
 
 std::vector<WorkUnit> build_units(const dcp_attn_desc* d, int tile, bool keys_major) {
   const int32_t* cu = d->cu_seqlens_host;
-  const size_t total = tiles_per_head(d, tile) * size_t(d->n_heads);
+  const int32_t H = d->n_heads;
+  const size_t total = tiles_per_head(d, tile) * size_t(H);
   std::vector<WorkUnit> out;
   if (total == 0) return out;
   const size_t cap = std::max<size_t>(4, (total + 8 * kNumXcd - 1) / (8 * kNumXcd));
-  struct Chunk {
-    int32_t b, h, t_begin, t_end;
+  // A chunk's work does not depend on its head, so the (sequence, chunk)
+  // groups are ordered (longest first) and each expands into its H chunks;
+  // thousands of short sequences then cost a sort of the groups only.
+  struct Group {
     int64_t work;
+    int32_t b, t_begin, t_end;
   };
-  std::vector<Chunk> chunks;
+  std::vector<Group> groups;
   auto tile_work = [&](int32_t len, int32_t t0, int32_t rows) -> int64_t {
     if (!d->causal) return len;
     return keys_major ? int64_t(len) - t0 : int64_t(t0) + rows;
@@ -127,35 +131,38 @@ std::vector<WorkUnit> build_units(const dcp_attn_desc* d, int tile, bool keys_ma
   for (int32_t b = 0; b < d->n_seqs; ++b) {
     const int32_t len = cu[b + 1] - cu[b];
     const int32_t nt = (len + tile - 1) / tile;
-    for (int32_t h = 0; h < d->n_heads; ++h)
-      for (int32_t c0 = 0; c0 < nt; c0 += int32_t(cap)) {
-        Chunk c{b, h, c0, std::min<int32_t>(nt, c0 + int32_t(cap)), 0};
-        for (int32_t t = c.t_begin; t < c.t_end; ++t)
-          c.work += tile_work(len, t * tile, std::min(tile, len - t * tile));
-        chunks.push_back(c);
-      }
+    for (int32_t c0 = 0; c0 < nt; c0 += int32_t(cap)) {
+      Group g{0, b, c0, std::min<int32_t>(nt, c0 + int32_t(cap))};
+      for (int32_t t = g.t_begin; t < g.t_end; ++t) g.work += tile_work(len, t * tile, std::min(tile, len - t * tile));
+      groups.push_back(g);
+    }
   }
-  std::stable_sort(chunks.begin(), chunks.end(), [](const Chunk& x, const Chunk& y) { return x.work > y.work; });
+  std::stable_sort(groups.begin(), groups.end(), [](const Group& x, const Group& y) { return x.work > y.work; });
   std::vector<std::vector<WorkUnit>> lists(kNumXcd);
+  for (auto& l : lists) l.reserve(total / kNumXcd + size_t(cap) + 1);
   int64_t load[kNumXcd] = {0};
-  for (const Chunk& c : chunks) {
-    int x = 0;
-    for (int i = 1; i < kNumXcd; ++i)
-      if (load[i] < load[x]) x = i;
-    load[x] += c.work;
-    const int32_t s0 = cu[c.b], len = cu[c.b + 1] - cu[c.b];
-    // within a chunk, the tile with the most work first (causal: the last
-    // query tiles of the forward, the first key tiles of the dK/dV pass)
-    const bool reverse = d->causal && !keys_major;
-    for (int32_t i = c.t_begin; i < c.t_end; ++i) {
-      const int32_t t = reverse ? c.t_end - 1 - (i - c.t_begin) : i;
-      WorkUnit u{};
-      u.row0 = s0 + t * tile;
-      u.rows = std::min(tile, len - t * tile);
-      u.seq0 = s0;
-      u.seqlen = len;
-      u.head = c.h;
-      lists[size_t(x)].push_back(u);
+  // within a chunk, the tile with the most work first (causal: the last
+  // query tiles of the forward, the first key tiles of the dK/dV pass)
+  const bool reverse = d->causal && !keys_major;
+  for (const Group& g : groups) {
+    const int32_t s0 = cu[g.b], len = cu[g.b + 1] - cu[g.b];
+    for (int32_t h = 0; h < H; ++h) {
+      // the least-loaded die takes the chunk
+      int x = 0;
+      for (int i = 1; i < kNumXcd; ++i)
+        if (load[i] < load[x]) x = i;
+      load[x] += g.work;
+      std::vector<WorkUnit>& l = lists[size_t(x)];
+      for (int32_t i = g.t_begin; i < g.t_end; ++i) {
+        const int32_t t = reverse ? g.t_end - 1 - (i - g.t_begin) : i;
+        WorkUnit u{};
+        u.row0 = s0 + t * tile;
+        u.rows = std::min(tile, len - t * tile);
+        u.seq0 = s0;
+        u.seqlen = len;
+        u.head = h;
+        l.push_back(u);
+      }
     }
   }
   size_t per = 0;
@@ -191,20 +198,20 @@ BwdLayout bwd_layout(const dcp_attn_desc* d) {
 // The constant block at the head of a workspace -- 16-byte chunks the
 // kernels' direct-to-LDS copies read for pad columns ([0 x 8] and
 // [1, 0 x 7] in bf16) and for rows past a sequence end (fp32 +inf) --
-// and the work lists after it, uploaded with one copy.  Each list goes to
-// its byte offset in the workspace.
+// and the work lists, each copied to its byte offset in the workspace
+// (one copy per list: the space reserved between them is not touched).
 int upload_head(std::initializer_list<std::pair<size_t, const std::vector<WorkUnit>*>> lists, void* dst,
                 hipStream_t stream) {
-  size_t bytes = kConstBytes;
-  for (const auto& l : lists) bytes = std::max(bytes, l.first + l.second->size() * sizeof(WorkUnit));
-  std::vector<unsigned char> buf(bytes, 0);
+  unsigned char head[kConstBytes] = {};
   const uint16_t one = 0x3F80;  // bf16 1.0
-  std::memcpy(buf.data() + kConstOnes * 2, &one, sizeof one);
+  std::memcpy(head + kConstOnes * 2, &one, sizeof one);
   const float inf = std::numeric_limits<float>::infinity();
-  std::memcpy(buf.data() + kConstInf * 2, &inf, sizeof inf);
+  std::memcpy(head + kConstInf * 2, &inf, sizeof inf);
+  hipError_t e = hipMemcpyAsync(dst, head, sizeof head, hipMemcpyHostToDevice, stream);
   for (const auto& l : lists)
-    if (!l.second->empty()) std::memcpy(buf.data() + l.first, l.second->data(), l.second->size() * sizeof(WorkUnit));
-  hipError_t e = hipMemcpyAsync(dst, buf.data(), buf.size(), hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess && !l.second->empty())
+      e = hipMemcpyAsync(static_cast<unsigned char*>(dst) + l.first, l.second->data(),
+                         l.second->size() * sizeof(WorkUnit), hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
   return DCP_OK;
 }

@@ -119,6 +119,36 @@ def video_long_tail_packs(rng: np.random.Generator, n_packs: int = 8, cap: int =
             for i, p in enumerate(packs[:n_packs])]
 
 
+def video_clips(rng: np.random.Generator, n_tokens: int, cap: int = 131072) -> List[tuple]:
+    """Clips (frames, tokens per frame) drawn like the long-tail mix until
+    their tokens reach ``n_tokens`` (clips above ``cap`` redrawn)."""
+    clips, tot = [], 0
+    while tot < n_tokens:
+        f = int(rng.choice(VIDEO_FRAMES, p=VIDEO_FRAME_WEIGHTS))
+        hgt, wid = VIDEO_RESOLUTIONS[int(rng.integers(0, len(VIDEO_RESOLUTIONS)))]
+        n = video_tokens_per_frame(hgt, wid)
+        if f * n > cap:
+            continue
+        clips.append((f, n))
+        tot += f * n
+    return clips
+
+
+def video_2d_pack(rng: np.random.Generator, axis: str, cap: int = 131072) -> Workload:
+    """Transformer-2D attention (Sec. 4.1; Table 1: 16 heads of width 72)
+    attends within one frame (spatial) or along one token position over
+    the frames (temporal): a clip of f frames x n tokens per frame is f
+    spatial sequences of n tokens or n temporal sequences of f tokens (a
+    single-frame clip gives sequences of one token).  Clips drawn like the
+    long-tail mix, sequences packed in clip order into <= cap tokens; the
+    first pack."""
+    lens: List[int] = []
+    for f, n in video_clips(rng, cap):
+        lens += [n] * f if axis == "spatial" else [f] * n
+    pack = greedy_pack(lens, cap)[0]
+    return Workload(f"video-DiT 2-D {axis} pack H16 D72", pack, 16, 72, False, 1.0 / math.sqrt(72))
+
+
 def ulysses_shard(length: int) -> Workload:
     """One device's Ulysses shard at SP=8 of a 16-head model: all tokens of a
     single sequence, 2 local heads of width 128."""
