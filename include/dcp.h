@@ -74,7 +74,7 @@ const char* dcp_version(void);
  *   cu_seqlens_host host int32 [n_seqs+1]: cu[0] = 0, non-decreasing,
  *                   cu[n_seqs] <= total_tokens.
  *   total_tokens    T, rows allocated in every [T, H, D] tensor, < 2^31.
- *   n_heads         H >= 1 (all heads share cu_seqlens).
+ *   n_heads         H in [1, 65535] (all heads share cu_seqlens).
  *   head_dim        D in {64, 72, 128}; anything else is DCP_ERR_UNSUPPORTED.
  *   scale           softmax scale applied to Q K^T, finite and > 0
  *                   (1/sqrt(D) in the usual models).

@@ -29,12 +29,12 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 // rows == 0 marks padding (the workgroup exits at once).
 struct WorkUnit {
   int32_t row0;
-  int32_t rows;
   int32_t seq0;
   int32_t seqlen;
-  int32_t head;
-  int32_t pad[3];
+  uint16_t rows;  // at most one tile (256)
+  uint16_t head;  // head counts are limited to 65535 by the C ABI
 };
+static_assert(sizeof(WorkUnit) == 16, "16 bytes per tile");
 
 constexpr int kNumXcd = 8;  // MI355X: 8 accelerator dies, each with its own L2
 

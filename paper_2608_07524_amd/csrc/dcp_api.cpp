@@ -72,7 +72,7 @@ int validate_desc(const dcp_attn_desc* d) {
   if (!d->cu_seqlens_host) return fail(DCP_ERR_INVALID, "cu_seqlens_host is null");
   if (d->total_tokens < 0 || d->total_tokens >= (int64_t(1) << 31))
     return fail(DCP_ERR_INVALID, "total_tokens must be in [0, 2^31)");
-  if (d->n_heads < 1) return fail(DCP_ERR_INVALID, "n_heads must be >= 1");
+  if (d->n_heads < 1 || d->n_heads > 65535) return fail(DCP_ERR_INVALID, "n_heads must be in [1, 65535]");
   if (d->head_dim != 64 && d->head_dim != 72 && d->head_dim != 128)
     return fail(DCP_ERR_UNSUPPORTED, "head_dim %d is not supported (64, 72, 128)", d->head_dim);
   if (!(std::isfinite(d->scale) && d->scale > 0.f)) return fail(DCP_ERR_INVALID, "scale must be finite and > 0");
@@ -157,10 +157,10 @@ std::vector<WorkUnit> build_units(const dcp_attn_desc* d, int tile, bool keys_ma
         const int32_t t = reverse ? g.t_end - 1 - (i - g.t_begin) : i;
         WorkUnit u{};
         u.row0 = s0 + t * tile;
-        u.rows = std::min(tile, len - t * tile);
+        u.rows = uint16_t(std::min(tile, len - t * tile));
         u.seq0 = s0;
         u.seqlen = len;
-        u.head = h;
+        u.head = uint16_t(h);
         l.push_back(u);
       }
     }

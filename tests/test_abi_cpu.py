@@ -43,6 +43,7 @@ def _desc(cu, T, H=2, D=64, scale=0.125, causal=0):
     (dict(cu=[0, 5, 3], T=5), N.DCP_ERR_INVALID),     # decreasing
     (dict(cu=[0, 9], T=5), N.DCP_ERR_INVALID),        # beyond total_tokens
     (dict(cu=[0, 5], T=5, H=0), N.DCP_ERR_INVALID),
+    (dict(cu=[0, 5], T=5, H=65536), N.DCP_ERR_INVALID),  # heads travel as uint16 in the work lists
     (dict(cu=[0, 5], T=5, D=96), N.DCP_ERR_UNSUPPORTED),
     (dict(cu=[0, 5], T=5, scale=0.0), N.DCP_ERR_INVALID),
     (dict(cu=[0, 5], T=5, scale=float("nan")), N.DCP_ERR_INVALID),
