@@ -123,6 +123,29 @@ int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, const void*
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The work the attention kernels run for `desc` (introspection for
+ * schedulers and tests: launches nothing, needs no GPU).  pass 0 is the
+ * forward, 1 the dK/dV pass, 2 the dQ pass.  Each unit is 5 int32
+ * {row0, seq0, seqlen, rows, head}: rows [row0, row0 + rows) of head `head`
+ * in the sequence occupying rows [seq0, seq0 + seqlen); rows == 0 is
+ * padding.  Units [0, *n_tiles) are such sequence tiles (tiles restart at
+ * every sequence start, so no block across two sequences is visited).  The
+ * rest are packed windows: runs of consecutive sequences, each shorter than
+ * a tile, sharing one tile of rows [row0, row0 + rows) (row0 == seq0), each
+ * row attending only within its own sequence; window w = -seqlen - 1 owns
+ * window_starts[4w .. 4w+3], where bit x % 64 of word x / 64 is set when a
+ * sequence starts at offset x of the window.  Each part is 8 consecutive
+ * per-die lists of equal length.
+ *   units          host int32 [cap][5], or NULL to query the counts only.
+ *   window_starts  host uint64 [cap_windows][4], or NULL.
+ *   n_units, n_tiles, n_windows  outputs (required).
+ * Returns DCP_ERR_INVALID for a bad desc or pass, or when a non-null array
+ * is too small (nothing is written then).
+ */
+int dcp_work_list(const dcp_attn_desc* desc, int32_t pass, int32_t* units, size_t cap, size_t* n_units,
+                  size_t* n_tiles, uint64_t* window_starts, size_t cap_windows, size_t* n_windows);
+
+/*
  * Instrumentation hook for profilers and benchmarks.  begin/end are
  * hipEvent_t handles (as void*) created by the caller.  While set on the
  * calling thread, every dcp_varlen_attn_fwd call records `begin` right

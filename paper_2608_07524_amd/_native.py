@@ -94,6 +94,8 @@ def load() -> C.CDLL:
         "dcp_varlen_attn_fwd": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp, sz, vp], C.c_int),
         "dcp_varlen_attn_bwd": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], C.c_int),
         "dcp_set_kernel_events": ([vp, vp], C.c_int),
+        "dcp_work_list": ([C.POINTER(AttnDesc), C.c_int32, C.POINTER(C.c_int32), sz, C.POINTER(sz), C.POINTER(sz),
+                           C.POINTER(C.c_uint64), sz, C.POINTER(sz)], C.c_int),
         "dcp_profile_workspace_size": ([C.c_int64, C.POINTER(ProfileOpts), C.POINTER(sz)], C.c_int),
         "dcp_profile_cost": ([C.POINTER(C.c_int64), C.c_int32, C.POINTER(ProfileOpts), vp, sz, vp,
                               C.POINTER(CostRow)], C.c_int),
@@ -253,6 +255,24 @@ def set_kernel_events(begin=None, end=None):
     dcp_set_kernel_events)."""
     _check(load().dcp_set_kernel_events(None if begin is None else C.c_void_p(begin),
                                         None if end is None else C.c_void_p(end)))
+
+
+def work_list(cu_seqlens, n_heads: int, head_dim: int, causal: bool, pass_: int):
+    """The tile list one kernel pass runs (0 forward, 1 dK/dV, 2 dQ; see
+    dcp_work_list): (units int32 [n, 5] = row0, seq0, seqlen, rows, head;
+    n_tiles, the count of sequence-tile units before the packed windows;
+    window_starts uint64 [n_windows, 4])."""
+    cu = np.asarray(cu_seqlens, dtype=np.int32)
+    d = _Desc(cu, int(cu[-1]), n_heads, head_dim, 1.0, causal)
+    lib = load()
+    n, nt, nw = C.c_size_t(), C.c_size_t(), C.c_size_t()
+    _check(lib.dcp_work_list(C.byref(d.desc), int(pass_), None, 0, C.byref(n), C.byref(nt), None, 0, C.byref(nw)))
+    units = np.zeros((max(n.value, 1), 5), dtype=np.int32)
+    starts = np.zeros((max(nw.value, 1), 4), dtype=np.uint64)
+    _check(lib.dcp_work_list(C.byref(d.desc), int(pass_), units.ctypes.data_as(C.POINTER(C.c_int32)), n.value,
+                             C.byref(n), C.byref(nt), starts.ctypes.data_as(C.POINTER(C.c_uint64)), nw.value,
+                             C.byref(nw)))
+    return units[:n.value], nt.value, starts[:nw.value]
 
 
 # ---------------------------------------------------------------------------

@@ -183,12 +183,13 @@ __device__ __forceinline__ void to_mfma16_layout(bf16x8& xv, bf16x8& yv) {
 // dP - Delta directly.  With KB = 2 every operand fetched from LDS feeds
 // two matrix products, and the exponentials of one key block can overlap
 // the products of the other.
-template <int D, int KB, int NW, int BM, int NSTAGE, int WPE, bool CAUSAL>
+template <int D, int KB, int NW, int BM, int NSTAGE, int WPE, bool CAUSAL, bool PACKED>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) void attn_bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
     __bf16* __restrict__ dk, __bf16* __restrict__ dv, const __bf16* __restrict__ consts,
-    const WorkUnit* __restrict__ units, int per_xcd, int H, int T, float scale, float scale_log2) {
+    const WorkUnit* __restrict__ units, const uint64_t* __restrict__ window_starts, int per_xcd, int H, int T,
+    float scale, float scale_log2) {
   using S = BwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
   constexpr int RSTR = S::DP + 8;  // an odd number of 16-byte chunks
@@ -218,7 +219,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   const int g = lane >> 5;
   const int j = lane & 31;
   const int64_t ts = int64_t(H) * D;
-  const int seqlen = u.seqlen;
+  constexpr bool packed = PACKED;  // a list of packed windows only
+  const int seqlen = packed ? int(u.rows) : u.seqlen;  // (window-relative offsets when packed)
   const int key_t0 = u.row0 - u.seq0;  // first key of the workgroup, sequence-relative
   const __bf16* zero = consts + kConstZero;
   const float* fzero = reinterpret_cast<const float*>(consts + kConstZero);
@@ -254,6 +256,16 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   wait_vmcnt<0>();  // settle the fragment loads before the first copy
 
   const int wave_key_lo = key_t0 + 32 * KB * wave;  // smallest key of this wavefront
+  // queries of each key's sequence: [q_lo, q_hi)
+  int q_lo[KB], q_hi[KB];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) {
+    q_lo[kb] = 0;
+    q_hi[kb] = seqlen;
+    if (packed)
+      window_bounds(window_starts + kWindowWords * (-u.seqlen - 1), min(wave_key_lo + 32 * kb + j, seqlen - 1),
+                    seqlen, q_lo[kb], q_hi[kb]);
+  }
   const int q_begin = CAUSAL ? (key_t0 / BM) * BM : 0;
   const int n_qt = (seqlen - q_begin + BM - 1) / BM;
 
@@ -263,7 +275,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   constexpr bool kFullCopies = !(CAUSAL && WPE == 1);
   const typename DR::FullOffsets fo_r = DR::full_offsets(ts, wave, lane);
   const typename DT::FullOffsets fo_t = DT::full_offsets(ts, wave, lane);
-  auto issue_tile = [&](int it) {
+  auto issue_tile = [&](int it) DCP_INLINE {
     const unsigned st = unsigned(it) % NSTAGE;
     const int q0 = q_begin + it * BM;
     const int valid = seqlen - q0;
@@ -284,7 +296,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
     DL::issue(&LV[st * 2 * BM], lseh + q0, ndh + q0, valid, finf, fzero, wave, lane);
   };
   // Waits until tile it+1 has landed (tile it+2 may stay in flight).
-  auto wait_next = [&](int it) {
+  auto wait_next = [&](int it) DCP_INLINE {
     if (NSTAGE == 3 && it + 2 < n_qt)
       wait_vmcnt<NI>();
     else
@@ -331,9 +343,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   const lds_f32* LV3 = lds_ptr(LV);
 
   // One 32-query block (first query qa, sequence-relative) of stage st
-  // against this wavefront's 32*KB keys.  MASK applies the causal mask.
-  auto process_block = [&](unsigned st, int qb, int qa, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
+  // against this wavefront's 32*KB keys.  MASK 1 applies the causal mask,
+  // 2 also each key's sequence bounds (packed windows).
+  auto process_block = [&](unsigned st, int qb, int qa, auto mask_tag) DCP_INLINE {
+    constexpr int MASK = decltype(mask_tag)::value;
     unsigned rb = st * RBUF + 32 * qb * RSTR + ar_off;
     unsigned tb = st * TBUF + 32 * qb * TSTR + tr_off;
     unsigned lb = st * 2 * BM + 32 * qb + 4 * g;
@@ -381,7 +394,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
         for (int c = 0; c < 4; ++c) {
           const int r = 4 * b + c;
           float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], scale_log2, -l4[b][c]));
-          if (MASK && key > qa + 8 * b + 4 * g + c) p = 0.f;
+          const int qq = qa + 8 * b + 4 * g + c;
+          if (MASK == 1 && key > qq) p = 0.f;
+          if (MASK == 2 && (unsigned(qq - q_lo[kb]) >= unsigned(q_hi[kb] - q_lo[kb]) || (CAUSAL && key > qq)))
+            p = 0.f;
           pa[kb][b >> 1][4 * (b & 1) + c] = __bf16(p);
           da[kb][b >> 1][4 * (b & 1) + c] = __bf16(p * dp[kb][r]);
         }
@@ -440,8 +456,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   // reaching its keys, where 32-query blocks entirely before its keys are
   // skipped and blocks crossing them masked, then those needing no mask.
   // Every iteration runs the same copy / wait / barrier sequence.
-  auto run = [&](int it0, int it1, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
+  // (packed windows: the queries of this wavefront's keys' sequences)
+  const int last_key = min(32 * KB - 1, int(u.rows) - 1 - 32 * KB * wave);  // of the wavefront, tile-relative
+  const int wq_lo = packed ? (CAUSAL ? wave_key_lo : __builtin_amdgcn_readfirstlane(q_lo[0])) : 0;
+  const int wq_hi = packed ? __builtin_amdgcn_readlane(q_hi[KB - 1], max(last_key, 0) % 32) : seqlen;
+  auto run = [&](int it0, int it1, auto mask_tag) DCP_INLINE {
+    constexpr int MASK = decltype(mask_tag)::value;
     for (int it = it0; it < it1; ++it) {
       if (it + NSTAGE - 1 < n_qt) issue_tile(it + NSTAGE - 1);
       const unsigned st = unsigned(it) % NSTAGE;
@@ -450,35 +470,48 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
       for (int qb = 0; qb < BM / 32; ++qb) {
         const int qa = q0 + 32 * qb;
         if (qa >= seqlen) continue;  // padding rows of the last tile
-        if (MASK) {
+        if (MASK == 1) {
           if (qa + 31 < wave_key_lo) continue;  // every query precedes every key
           if (qa >= wave_key_lo + 32 * KB - 1) {
-            process_block(st, qb, qa, std::false_type{});
+            process_block(st, qb, qa, std::integral_constant<int, 0>{});
             continue;
           }
         }
-        process_block(st, qb, qa, std::integral_constant<bool, MASK>{});
+        if (MASK == 2 && (qa + 31 < wq_lo || qa >= wq_hi)) continue;  // no query of these keys' sequences
+        process_block(st, qb, qa, std::integral_constant<int, MASK>{});
       }
       wait_next(it);
       __syncthreads();
     }
   };
-  if (32 * KB * wave < u.rows) {
-    int it_plain = 0;
-    if (CAUSAL) {
-      // first tile whose queries all follow all of this wavefront's keys
-      it_plain = min(n_qt, max(0, (wave_key_lo + 32 * KB - 1 - q_begin + BM - 1) / BM));
-      run(0, it_plain, std::true_type{});
-    }
-    run(it_plain, n_qt, std::false_type{});
-  } else {
-    // no key of the tile (the last tile of a sequence): copies and barriers only
-    for (int it = 0; it < n_qt; ++it) {
+  // no key of this wavefront in the tile: copies and barriers only
+  auto idle = [&](int it0, int it1) DCP_INLINE {
+    for (int it = it0; it < it1; ++it) {
       if (it + NSTAGE - 1 < n_qt) issue_tile(it + NSTAGE - 1);
       wait_next(it);
       __syncthreads();
     }
+  };
+  if (32 * KB * wave < u.rows) {
+    if constexpr (packed) {
+      const int it_lo = (wq_lo - q_begin) / BM;
+      const int it_hi = min(n_qt, (wq_hi - q_begin + BM - 1) / BM);
+      idle(0, it_lo);
+      run(it_lo, it_hi, std::integral_constant<int, 2>{});
+      idle(it_hi, n_qt);
+    } else {
+      int it_plain = 0;
+      if (CAUSAL) {
+        // first tile whose queries all follow all of this wavefront's keys
+        it_plain = min(n_qt, max(0, (wave_key_lo + 32 * KB - 1 - q_begin + BM - 1) / BM));
+        run(0, it_plain, std::integral_constant<int, 1>{});
+      }
+      run(it_plain, n_qt, std::integral_constant<int, 0>{});
+    }
+  } else {
+    idle(0, n_qt);  // no key of the tile (the last tile of a sequence)
   }
+
 
   // Epilogue through LDS (the ring is idle now): the workgroup's first half
   // of 32-key blocks is staged in the Q buffers, the second in the dO
@@ -509,12 +542,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
 // through an NSTAGE-deep LDS ring filled by direct global-to-LDS copies
 // NSTAGE - 1 tiles ahead (K twice: rows read 16 B per lane for S^T, rows
 // read by transposing reads for dQ^T; V once), one barrier per tile.
-template <int D, int NW, int NSTAGE, bool CAUSAL>
+template <int D, int NW, int NSTAGE, bool CAUSAL, bool PACKED>
 __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
-    __bf16* __restrict__ dq, const __bf16* __restrict__ consts, const WorkUnit* __restrict__ units, int per_xcd,
-    int H, int T, float scale, float scale_log2) {
+    __bf16* __restrict__ dq, const __bf16* __restrict__ consts, const WorkUnit* __restrict__ units,
+    const uint64_t* __restrict__ window_starts, int per_xcd, int H, int T, float scale, float scale_log2) {
   using S = BwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
   constexpr int KSTR = S::DP + 8;  // K and V rows read 16 B per lane
@@ -539,7 +572,8 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   const int g = lane >> 5;
   const int j = lane & 31;
   const int64_t ts = int64_t(H) * D;
-  const int seqlen = u.seqlen;
+  constexpr bool packed = PACKED;  // a list of packed windows only
+  const int seqlen = packed ? int(u.rows) : u.seqlen;  // (window-relative offsets when packed)
   const int tile_q0 = u.row0 - u.seq0;
   const int wave_q0 = tile_q0 + 32 * wave;
   const __bf16* zero = consts + kConstZero;
@@ -553,6 +587,10 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   const int qrel = 32 * wave + j;
   const bool q_ok = qrel < u.rows;
   const int my_q = tile_q0 + qrel;  // sequence-relative
+  // keys of this lane's sequence: [k_lo, k_hi)
+  int k_lo = 0, k_hi = seqlen;
+  if (packed)
+    window_bounds(window_starts + kWindowWords * (-u.seqlen - 1), min(my_q, seqlen - 1), seqlen, k_lo, k_hi);
   bf16x8 qf[NKD], df[NKD];
 #pragma unroll
   for (int kd = 0; kd < NKD; ++kd) {
@@ -581,7 +619,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
 
   const typename DK::FullOffsets fo_k = DK::full_offsets(ts, wave, lane);
   const typename DT::FullOffsets fo_t = DT::full_offsets(ts, wave, lane);
-  auto issue_tile = [&](int kt) {
+  auto issue_tile = [&](int kt) DCP_INLINE {
     const unsigned st = unsigned(kt) % NSTAGE;
     const int valid = seqlen - kt * BN;
     const __bf16* ks = kh + int64_t(kt) * BN * ts;
@@ -598,7 +636,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   // Before the barrier that ends tile kt: tile kt+1 must have landed; only
   // tile kt+2's copies (three stages: issued this iteration) may still be
   // in flight.
-  auto wait_next = [&](int kt) {
+  auto wait_next = [&](int kt) DCP_INLINE {
     if (NSTAGE == 3 && kt + 2 < n_tiles)
       wait_vmcnt<NI>();
     else
@@ -634,7 +672,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
 
   // One key tile against this wavefront's 32 queries.  MASK covers tiles
   // crossing the sequence end or the causal diagonal.
-  auto process_tile = [&](unsigned st, int k0, auto mask_tag) {
+  auto process_tile = [&](unsigned st, int k0, auto mask_tag) DCP_INLINE {
     constexpr bool MASK = decltype(mask_tag)::value;
     unsigned rb = st * KBUF + ar_off;
     unsigned tb = st * TBUF + tr_off;
@@ -666,7 +704,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
         float p = __builtin_amdgcn_exp2f(fmaf(s[kb][r], scale_log2, -lse_l2));
         if constexpr (MASK) {
           const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (key >= seqlen || (CAUSAL && key > my_q)) p = 0.f;
+          if (unsigned(key - k_lo) >= unsigned(k_hi - k_lo) || (CAUSAL && key > my_q)) p = 0.f;
         }
         dsb[kb][r >> 3][r & 7] = __bf16(p * (FOLD ? dp[kb][r] : dp[kb][r] + ndlt));
       }
@@ -705,15 +743,24 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
 
   // Key tiles in up to three phases per wavefront (unmasked, masked, idle),
   // each with the same copy / wait / barrier sequence.  A wavefront holding
-  // no query of the tile (the last tile of a sequence) only idles.
+  // no query of the tile (the last tile of a sequence) only idles.  In a
+  // packed window every tile is masked, and the tiles before the first
+  // query's sequence (t_lead) and after the last one's are idle.
+  int t_lead = 0;
   int t_mask = min(n_tiles, seqlen / BN);
   int t_idle = n_tiles;
   if (CAUSAL) {
     t_mask = min(t_mask, (wave_q0 + 1) / BN);
     t_idle = min(n_tiles, wave_last_q / BN + 1);
   }
-  if (32 * wave >= u.rows) t_mask = t_idle = 0;
-  auto run = [&](int kt0, int kt1, auto mode_tag) {
+  if constexpr (packed) {
+    const int last = min(31, int(u.rows) - 1 - 32 * wave);  // lane of the wavefront's last query
+    const int keys_end = min(__builtin_amdgcn_readlane(k_hi, max(last, 0)), CAUSAL ? wave_q0 + 32 : seqlen);
+    t_lead = t_mask = __builtin_amdgcn_readfirstlane(k_lo) / BN;
+    t_idle = min(n_tiles, (keys_end + BN - 1) / BN);
+  }
+  if (32 * wave >= u.rows) t_lead = t_mask = t_idle = 0;
+  auto run = [&](int kt0, int kt1, auto mode_tag) DCP_INLINE {
     constexpr int MODE = decltype(mode_tag)::value;  // 0 unmasked, 1 masked, 2 idle
     for (int kt = kt0; kt < kt1; ++kt) {
       if (kt + NSTAGE - 1 < n_tiles) issue_tile(kt + NSTAGE - 1);
@@ -724,7 +771,8 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
       __syncthreads();
     }
   };
-  run(0, t_mask, std::integral_constant<int, 0>{});
+  run(0, t_lead, std::integral_constant<int, 2>{});
+  run(t_lead, t_mask, std::integral_constant<int, 0>{});
   run(t_mask, t_idle, std::integral_constant<int, 1>{});
   run(t_idle, n_tiles, std::integral_constant<int, 2>{});
 
@@ -766,6 +814,32 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   }
 }
 
+template <int D, bool CAUSAL, bool PACKED>
+hipError_t launch_dkdv_list(const BwdArgs& a, const WorkUnit* units, int n_units) {
+  constexpr DkdvShape sh = bwd_dkdv_shape(D);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, sh.kb, sh.waves, sh.bm, sh.stages, sh.waves_per_eu, CAUSAL, PACKED>),
+                     dim3(n_units), dim3(64 * sh.waves), 0, a.stream, static_cast<const __bf16*>(a.q),
+                     static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
+                     static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dk),
+                     static_cast<__bf16*>(a.dv), static_cast<const __bf16*>(a.consts), units,
+                     static_cast<const uint64_t*>(a.window_starts), n_units / kNumXcd, a.n_heads, a.total_tokens,
+                     a.scale, a.scale * kLog2e);
+  return hipGetLastError();
+}
+
+template <int D, bool CAUSAL, bool PACKED>
+hipError_t launch_dq_list(const BwdArgs& a, const WorkUnit* units, int n_units) {
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, kBwdDqWaves, (D > 96 ? 2 : 3), CAUSAL, PACKED>), dim3(n_units),
+                     dim3(64 * kBwdDqWaves), 0, a.stream, static_cast<const __bf16*>(a.q),
+                     static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
+                     static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dq),
+                     static_cast<const __bf16*>(a.consts), units, static_cast<const uint64_t*>(a.qwindow_starts),
+                     n_units / kNumXcd, a.n_heads, a.total_tokens, a.scale, a.scale * kLog2e);
+  return hipGetLastError();
+}
+
+// Delta, then the dK/dV pass and the dQ pass, each over its sequence tiles
+// and then its packed windows (one launch per non-empty list).
 template <int D, bool CAUSAL>
 hipError_t launch_bwd_t(const BwdArgs& a) {
   const int64_t n_pairs = int64_t(a.rows_end) * a.n_heads;
@@ -778,30 +852,19 @@ hipError_t launch_bwd_t(const BwdArgs& a) {
     if (e != hipSuccess) return e;
   }
   const KernelEvents& ev = kernel_events();
-  if (a.n_units > 0) {
+  const WorkUnit* units = static_cast<const WorkUnit*>(a.units);
+  const WorkUnit* qunits = static_cast<const WorkUnit*>(a.qunits);
+  hipError_t e = hipSuccess;
+  if (a.n_units + a.n_wunits > 0) {
     if (ev.begin) (void)hipEventRecord(ev.begin, a.stream);
-    constexpr DkdvShape sh = bwd_dkdv_shape(D);
-    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, sh.kb, sh.waves, sh.bm, sh.stages, sh.waves_per_eu, CAUSAL>), dim3(a.n_units), dim3(64 * sh.waves), 0, a.stream, static_cast<const __bf16*>(a.q),
-                       static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
-                       static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dk),
-                       static_cast<__bf16*>(a.dv), static_cast<const __bf16*>(a.consts),
-                       static_cast<const WorkUnit*>(a.units), a.n_units / kNumXcd, a.n_heads, a.total_tokens, a.scale,
-                       a.scale * kLog2e);
-    hipError_t e = hipGetLastError();
+    if (a.n_units > 0) e = launch_dkdv_list<D, CAUSAL, false>(a, units, a.n_units);
+    if (e == hipSuccess && a.n_wunits > 0) e = launch_dkdv_list<D, CAUSAL, true>(a, units + a.n_units, a.n_wunits);
     if (ev.end) (void)hipEventRecord(ev.end, a.stream);
     if (e != hipSuccess) return e;
   }
-  if (a.n_qunits > 0) {
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, kBwdDqWaves, (D > 96 ? 2 : 3), CAUSAL>), dim3(a.n_qunits),
-                       dim3(64 * kBwdDqWaves), 0, a.stream, static_cast<const __bf16*>(a.q),
-                       static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
-                       static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dq),
-                       static_cast<const __bf16*>(a.consts), static_cast<const WorkUnit*>(a.qunits), a.n_qunits / kNumXcd, a.n_heads, a.total_tokens, a.scale,
-                       a.scale * kLog2e);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
+  if (a.n_qunits > 0) e = launch_dq_list<D, CAUSAL, false>(a, qunits, a.n_qunits);
+  if (e == hipSuccess && a.n_wqunits > 0) e = launch_dq_list<D, CAUSAL, true>(a, qunits + a.n_qunits, a.n_wqunits);
+  return e;
 }
 
 // Deterministic fill for profiling inputs: a 32-bit integer hash mapped to

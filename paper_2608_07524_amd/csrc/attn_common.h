@@ -27,6 +27,11 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 // One tile of work: rows [row0, row0 + rows) of the packed tensor for head
 // `head`, all in the sequence that occupies rows [seq0, seq0 + seqlen).
 // rows == 0 marks padding (the workgroup exits at once).
+// A negative seqlen marks a packed window instead: consecutive sequences,
+// each shorter than a tile, sharing one tile of `rows` rows that starts at
+// row0 == seq0.  Row i of the window attends only to rows of its own
+// sequence; -seqlen - 1 indexes the window's mask of sequence starts (four
+// 64-bit words, bit x set where a sequence starts at window offset x).
 struct WorkUnit {
   int32_t row0;
   int32_t seq0;
@@ -35,6 +40,29 @@ struct WorkUnit {
   uint16_t head;  // head counts are limited to 65535 by the C ABI
 };
 static_assert(sizeof(WorkUnit) == 16, "16 bytes per tile");
+constexpr int kWindowWords = 4;  // 64-bit words per window mask: windows hold at most 256 rows
+
+// Bounds [lo, hi) of the sequence holding window offset x (0 <= x < n,
+// the window's length), from the window's mask of sequence starts (bit 0
+// is always set).
+__device__ __forceinline__ void window_bounds(const uint64_t* __restrict__ starts, int x, int n, int& lo,
+                                              int& hi) {
+  lo = 0;
+  hi = n;
+#pragma unroll
+  for (int w = 0; w < kWindowWords; ++w) {
+    const uint64_t m = starts[w];
+    const int r = x - 64 * w;  // x's bit in word w (outside 0..63 when x is in another word)
+    const uint64_t upto = r < 0 ? 0ull : (r >= 63 ? ~0ull : (2ull << r) - 1);
+    const uint64_t le = m & upto, gt = m & ~upto;  // starts at or before x, after x
+    if (le) lo = 64 * w + 63 - __builtin_clzll(le);  // words ascend: the last hit is the nearest
+    if (gt) hi = min(hi, 64 * w + __builtin_ctzll(gt));
+  }
+}
+
+// Kernel-local lambdas are always inlined: a call would need a stack frame
+// (scratch memory) and spill the caller's live registers around it.
+#define DCP_INLINE __attribute__((always_inline))
 
 constexpr int kNumXcd = 8;  // MI355X: 8 accelerator dies, each with its own L2
 

@@ -45,6 +45,7 @@ constexpr int kFwdBN = 64;
 constexpr int kFwdStages = DCP_FWD_STAGES;
 static_assert(kFwdStages >= 3, "tiles kt and kt + 1 are read while kt + 2 lands");
 constexpr float kRescaleSlack = 8.0f;  // log2 units
+constexpr float kNoMax = -1e30f;       // running max before any key
 
 template <int D>
 struct FwdShape {
@@ -72,14 +73,15 @@ constexpr int kSchedMfma = 0x008;
 constexpr int kSchedValu = 0x002;
 constexpr int kSchedDsRead = 0x100;
 
-template <int D, int NW, bool CAUSAL>
+template <int D, int NW, bool CAUSAL, bool PACKED>
 __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restrict__ q,
                                                            const __bf16* __restrict__ k,
                                                            const __bf16* __restrict__ v, __bf16* __restrict__ o,
                                                            float* __restrict__ lse,
                                                            const __bf16* __restrict__ consts,
-                                                           const WorkUnit* __restrict__ units, int per_xcd, int H, int T,
-                                                           float scale_log2) {
+                                                           const WorkUnit* __restrict__ units,
+                                                           const uint64_t* __restrict__ window_starts, int per_xcd,
+                                                           int H, int T, float scale_log2) {
   using S = FwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, KSTR = S::KSTR, VSTR = S::VSTR, CPR = S::CPR;
   constexpr int BN = kFwdBN;
@@ -114,8 +116,12 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
 
   const int tile_q0 = u.row0 - u.seq0;  // first query of the tile, sequence-relative
   const int wave_q0 = tile_q0 + wave * 32;
-  const int seqlen = u.seqlen;
+  constexpr bool packed = PACKED;  // a list of packed windows only
+  const int seqlen = packed ? int(u.rows) : u.seqlen;  // (window-relative offsets when packed)
   const int qi = wave_q0 + j;  // this lane's query
+  // keys of this lane's sequence: [k_lo, k_hi)
+  int k_lo = 0, k_hi = seqlen;
+  if (packed) window_bounds(window_starts + kWindowWords * (-u.seqlen - 1), min(qi, seqlen - 1), seqlen, k_lo, k_hi);
 
   // Q fragments (B operand of S^T): lane (g, j) holds query j,
   // columns 16*kd + 8*g .. +7.
@@ -144,11 +150,17 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   // up to t_work tiles with masking on (a block past the wavefront's keys is
   // simply fully masked), then idles to n_tiles so that every wavefront
   // meets the same barriers.  A wavefront holding no query of the tile
-  // (the last tile of a sequence) only copies and idles.
+  // (the last tile of a sequence) only copies and idles.  In a packed
+  // window every block is masked, and the wavefront first idles through
+  // the tiles before its first query's sequence (t_first).
   const bool live = wave * 32 < u.rows;
-  const int wave_keys = CAUSAL ? min(seqlen, wave_q0 + 32) : seqlen;
+  const int last = min(31, int(u.rows) - 1 - wave * 32);  // lane of the wavefront's last query
+  const int wave_keys = packed ? min(__builtin_amdgcn_readlane(k_hi, max(last, 0)), CAUSAL ? wave_q0 + 32 : seqlen)
+                               : (CAUSAL ? min(seqlen, wave_q0 + 32) : seqlen);
+  const int t_first = packed && live ? __builtin_amdgcn_readfirstlane(k_lo) / BN : 0;
+  const int b_first = 2 * t_first;
   const int nb = live ? min((wave_keys + 31) / 32, 2 * n_tiles) : 0;
-  const int b_mask = min(nb, CAUSAL ? min(seqlen / 32, (wave_q0 + 1) / 32) : seqlen / 32);
+  const int b_mask = packed ? 0 : min(nb, CAUSAL ? min(seqlen / 32, (wave_q0 + 1) / 32) : seqlen / 32);
   const int t_work = (nb + 1) / 2;
   const int t_plain = b_mask >= 1 ? (b_mask - 1) / 2 : 0;  // tiles kt with 2kt + 2 < b_mask
 
@@ -166,7 +178,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
           bf16x8{__bf16(1.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f)};
     }
   }
-  auto issue_tile = [&](int kt) {
+  auto issue_tile = [&](int kt) DCP_INLINE {
     const unsigned st = unsigned(kt) % NST;
     const int valid = min(BN, seqlen - kt * BN);
     if (valid == BN) {
@@ -185,7 +197,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   // scores of tile kt + 1's first block are computed while tile kt is
   // processed); copies of the tiles after them may still be in flight.
   constexpr int PD = NST - 1;  // prefetch distance in tiles
-  auto wait_for = [&](int kt) {
+  auto wait_for = [&](int kt) DCP_INLINE {
     const int ahead = min(PD - 2, n_tiles - kt - 2);  // tiles issued beyond kt + 1
     if (PD >= 4 && ahead >= 2) {
       wait_vmcnt<(PD >= 4 ? 2 * NI : 0)>();
@@ -209,7 +221,10 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   const lds_bf16* Ks3 = lds_ptr(Ks);
   const lds_bf16* Vs3 = lds_ptr(Vs);
 
-  float m_use = -INFINITY, l_run = 0.f;
+  // Finite start: a row whose first blocks are all masked (packed windows)
+  // then gets exp2(-inf + kNoMax) = 0 there, not NaN; its first key moves
+  // m with a factor exp2(kNoMax - m) = 0 on the empty accumulators.
+  float m_use = kNoMax, l_run = 0.f;
   f32x16 oacc[NDB];  // O^T in 32-row blocks (lane (g, j): query j)
 #pragma unroll
   for (int db = 0; db < NDB; ++db) oacc[db] = f32x16{};
@@ -221,27 +236,27 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   for (int mb = 0; mb < NMB; ++mb) oacc16[mb][0] = oacc16[mb][1] = f32x4{};
 
   // S^T of one 32-key block whose K rows start at LDS element kbase.
-  auto scores = [&](unsigned kbase) {
+  auto scores = [&](unsigned kbase) DCP_INLINE {
     f32x16 s = f32x16{};
 #pragma unroll
     for (int kd = 0; kd < NKD; ++kd) s = mfma32(lds_read_b128(Ks3 + kbase + 16 * kd), qf[kd], s);
     return s;
   };
-  auto apply_mask = [&](f32x16& s, int b) {
+  auto apply_mask = [&](f32x16& s, int b) DCP_INLINE {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int key = 32 * b + 8 * (r >> 2) + 4 * g + (r & 3);
-      if (key >= seqlen || (CAUSAL && key > qi)) s[r] = -INFINITY;
+      if (unsigned(key - k_lo) >= unsigned(k_hi - k_lo) || (CAUSAL && key > qi)) s[r] = -INFINITY;
     }
   };
-  auto row_max = [&](const f32x16& s) {
+  auto row_max = [&](const f32x16& s) DCP_INLINE {
     float t = -INFINITY;  // a sequential chain lowers to v_max3
 #pragma unroll
     for (int r = 0; r < 16; ++r) t = fmaxf(t, s[r]);
     return half_swap_max(t) * scale_log2;
   };
   // Lazy rescale: move m only when the row max outgrows it by > 2^8.
-  auto rescale = [&](float mx, bool valid) {
+  auto rescale = [&](float mx, bool valid) DCP_INLINE {
     if (__builtin_amdgcn_ballot_w64(valid && mx > m_use + kRescaleSlack)) {
       const float m_new = fmaxf(m_use, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_use - m_new);  // 0 on the first block
@@ -305,12 +320,21 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   wait_for(0);
   __syncthreads();
 
+  // A tile this wavefront has no work in: its copies, wait and barrier.
+  auto idle = [&](int kt) DCP_INLINE {
+    if (kt + PD < n_tiles) issue_tile(kt + PD);
+    wait_for(kt + 1);
+    __syncthreads();
+  };
+  int kt = 0;
+  for (; kt < t_first; ++kt) idle(kt);
+
   f32x16 sc{};  // S^T of the current block, masked, not yet exponentiated
-  if (nb > 0) {
-    unsigned kb0 = kr_off;
+  if (nb > b_first) {
+    unsigned kb0 = (unsigned(t_first) % NST) * KBUF + kr_off;
     asm("" : "+v"(kb0));
     sc = scores(kb0);
-    if (b_mask == 0) apply_mask(sc, 0);
+    if (b_mask <= b_first) apply_mask(sc, b_first);
     rescale(row_max(sc), true);
   }
 
@@ -318,7 +342,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   // while the scores of block bn (K rows at knext) are computed, masked
   // when MASK, and their row max taken.  On a wavefront's last block the
   // successor's scores are computed but not used (valid_next false).
-  auto step = [&](int bn, unsigned knext, unsigned vcur, bool valid_next, auto mask_tag) {
+  auto step = [&](int bn, unsigned knext, unsigned vcur, bool valid_next, auto mask_tag) DCP_INLINE {
     constexpr bool MASK = decltype(mask_tag)::value;
     f32x16 sn = scores(knext);
     // P = exp2(S*scale*log2e - m) as bf16 (B operand of the PV product)
@@ -357,7 +381,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
 
   // Tile kt: blocks 2kt and 2kt + 1; the successor of the second block is
   // the first block of tile kt + 1.
-  auto tile = [&](int kt, auto mask_tag) {
+  auto tile = [&](int kt, auto mask_tag) DCP_INLINE {
     if (kt + PD < n_tiles) issue_tile(kt + PD);
     unsigned kb0 = (unsigned(kt) % NST) * KBUF + kr_off;
     unsigned kb1 = (unsigned(kt + 1) % NST) * KBUF + kr_off;
@@ -368,14 +392,9 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
     wait_for(kt + 1);
     __syncthreads();
   };
-  int kt = 0;
   for (; kt < t_plain; ++kt) tile(kt, std::false_type{});
   for (; kt < t_work; ++kt) tile(kt, std::true_type{});
-  for (; kt < n_tiles; ++kt) {
-    if (kt + PD < n_tiles) issue_tile(kt + PD);
-    wait_for(kt + 1);
-    __syncthreads();
-  }
+  for (; kt < n_tiles; ++kt) idle(kt);
 
   // Epilogue.
   if constexpr (S::PV16) {
@@ -441,18 +460,25 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   }
 }
 
-template <int D, int NW, bool CAUSAL>
-hipError_t launch_fwd_t(const FwdArgs& a) {
-  dim3 grid(a.n_units);
-  const KernelEvents& ev = kernel_events();
-  if (ev.begin) (void)hipEventRecord(ev.begin, a.stream);
-  hipLaunchKernelGGL((attn_fwd_kernel<D, NW, CAUSAL>), grid, dim3(64 * NW), 0, a.stream,
+template <int D, int NW, bool CAUSAL, bool PACKED>
+hipError_t launch_fwd_list(const FwdArgs& a, const WorkUnit* units, int n_units) {
+  hipLaunchKernelGGL((attn_fwd_kernel<D, NW, CAUSAL, PACKED>), dim3(n_units), dim3(64 * NW), 0, a.stream,
                      static_cast<const __bf16*>(a.q), static_cast<const __bf16*>(a.k),
                      static_cast<const __bf16*>(a.v), static_cast<__bf16*>(a.o), a.lse,
-                     static_cast<const __bf16*>(a.consts), static_cast<const WorkUnit*>(a.units),
-                     a.n_units / kNumXcd, a.n_heads, a.total_tokens,
-                     a.scale * kLog2e);
-  hipError_t e = hipGetLastError();
+                     static_cast<const __bf16*>(a.consts), units, static_cast<const uint64_t*>(a.window_starts),
+                     n_units / kNumXcd, a.n_heads, a.total_tokens, a.scale * kLog2e);
+  return hipGetLastError();
+}
+
+// Sequence tiles, then packed windows: one launch per non-empty list.
+template <int D, int NW, bool CAUSAL>
+hipError_t launch_fwd_t(const FwdArgs& a) {
+  const KernelEvents& ev = kernel_events();
+  const WorkUnit* units = static_cast<const WorkUnit*>(a.units);
+  if (ev.begin) (void)hipEventRecord(ev.begin, a.stream);
+  hipError_t e = hipSuccess;
+  if (a.n_units > 0) e = launch_fwd_list<D, NW, CAUSAL, false>(a, units, a.n_units);
+  if (e == hipSuccess && a.n_wunits > 0) e = launch_fwd_list<D, NW, CAUSAL, true>(a, units + a.n_units, a.n_wunits);
   if (ev.end) (void)hipEventRecord(ev.end, a.stream);
   return e;
 }
@@ -462,7 +488,7 @@ hipError_t launch_fwd_t(const FwdArgs& a) {
 int fwd_tile_rows(int head_dim) { return kFwdWaves * 32; }
 
 hipError_t launch_fwd(const FwdArgs& a) {
-  if (a.n_units == 0) return hipSuccess;
+  if (a.n_units == 0 && a.n_wunits == 0) return hipSuccess;
   constexpr int W = kFwdWaves;
   switch (a.head_dim) {
     case 64: return a.causal ? launch_fwd_t<64, W, true>(a) : launch_fwd_t<64, W, false>(a);

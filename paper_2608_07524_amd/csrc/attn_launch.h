@@ -58,8 +58,11 @@ struct FwdArgs {
   void* o;
   float* lse;
   const void* consts;  // device: the 16-byte constant chunks (workspace head)
-  const void* units;   // device WorkUnit[n_units], 8 per-die lists of n_units / 8
+  const void* units;   // device WorkUnit[n_units + n_wunits]: sequence tiles, then packed windows,
+                       // each part 8 per-die lists
+  const void* window_starts;  // device: 4 uint64 per packed window
   int n_units;
+  int n_wunits;
   int n_heads;
   int head_dim;
   int total_tokens;
@@ -81,10 +84,14 @@ struct BwdArgs {
   float* ndelta;          // fp32 [H, T] workspace: -rowsum(dO o O)
   float* lse2;            // fp32 [H, T] workspace: LSE * log2(e)
   const void* consts;     // device: the 16-byte constant chunks (workspace head)
-  const void* units;      // device WorkUnit[n_units], key tiles (8 per-die lists)
+  const void* units;      // device WorkUnit[n_units + n_wunits], key tiles then packed windows
+  const void* window_starts;   // device: 4 uint64 per packed window of the key-tile list
   int n_units;
-  const void* qunits;     // device WorkUnit[n_qunits], query tiles (8 per-die lists)
+  int n_wunits;
+  const void* qunits;     // device WorkUnit[n_qunits + n_wqunits], query tiles then packed windows
+  const void* qwindow_starts;  // device: the same for the query-tile list
   int n_qunits;
+  int n_wqunits;
   int rows_end;           // cu_seqlens[n]: rows past it are not touched
   int n_heads;
   int head_dim;

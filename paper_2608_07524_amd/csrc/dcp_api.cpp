@@ -95,13 +95,17 @@ int check_tensor(const void* p, const char* name) {
 }
 
 // Tiles of `tile` rows per (sequence, head), never straddling two
-// sequences, laid out as 8 per-die lists (see unit_for_block).  Work of a
-// tile: the keys it visits (forward, dQ pass) or the queries visiting it
-// (dK/dV pass).  The (sequence, head) groups -- split into chunks when a
-// few long sequences would otherwise leave dies idle -- are assigned to the
-// least-loaded die, longest first; each die's list keeps a chunk's tiles
-// together (they share K/V or Q/dO in that die's L2) and is padded with
-// empty tiles to the longest list.
+// sequences, laid out as 8 per-die lists (see unit_for_block).  Runs of
+// consecutive sequences shorter than a tile share one tile as a packed
+// window of at most `tile` rows (each row still attends only within its
+// own sequence), so thousands of short sequences do not each occupy a
+// mostly idle workgroup.  Work of a tile: the keys it visits (forward, dQ
+// pass) or the queries visiting it (dK/dV pass); a window's is its row
+// count.  The (sequence, chunk) and window groups -- long sequences split
+// into chunks when a few of them would otherwise leave dies idle -- are
+// assigned to the least-loaded die, longest first; each die's list keeps a
+// chunk's tiles together (they share K/V or Q/dO in that die's L2) and is
+// padded with empty tiles to the longest list.
 size_t tiles_per_head(const dcp_attn_desc* d, int tile) {
   size_t n = 0;
   for (int32_t b = 0; b < d->n_seqs; ++b)
@@ -109,67 +113,121 @@ size_t tiles_per_head(const dcp_attn_desc* d, int tile) {
   return n;
 }
 
-std::vector<WorkUnit> build_units(const dcp_attn_desc* d, int tile, bool keys_major) {
+struct UnitList {
+  std::vector<WorkUnit> units;  // n_tiles sequence tiles, then the packed windows (8 per-die lists each)
+  size_t n_tiles = 0;
+  std::vector<uint64_t> window_starts;  // kWindowWords per packed window
+};
+
+UnitList build_units(const dcp_attn_desc* d, int tile, bool keys_major) {
   const int32_t* cu = d->cu_seqlens_host;
   const int32_t H = d->n_heads;
+  const int32_t n = d->n_seqs;
+  UnitList out;
   const size_t total = tiles_per_head(d, tile) * size_t(H);
-  std::vector<WorkUnit> out;
   if (total == 0) return out;
   const size_t cap = std::max<size_t>(4, (total + 8 * kNumXcd - 1) / (8 * kNumXcd));
-  // A chunk's work does not depend on its head, so the (sequence, chunk)
-  // groups are ordered (longest first) and each expands into its H chunks;
-  // thousands of short sequences then cost a sort of the groups only.
+  // A chunk's work does not depend on its head, so the groups are ordered
+  // (longest first) and each expands into its H chunks; thousands of short
+  // sequences then cost a sort of the groups only.
   struct Group {
     int64_t work;
     int32_t b, t_begin, t_end;
+    int32_t window;  // >= 0: packed window number (b: its first sequence, t_end: its rows)
   };
   std::vector<Group> groups;
   auto tile_work = [&](int32_t len, int32_t t0, int32_t rows) -> int64_t {
     if (!d->causal) return len;
     return keys_major ? int64_t(len) - t0 : int64_t(t0) + rows;
   };
-  for (int32_t b = 0; b < d->n_seqs; ++b) {
+  auto add_sequence = [&](int32_t b) {
     const int32_t len = cu[b + 1] - cu[b];
     const int32_t nt = (len + tile - 1) / tile;
     for (int32_t c0 = 0; c0 < nt; c0 += int32_t(cap)) {
-      Group g{0, b, c0, std::min<int32_t>(nt, c0 + int32_t(cap))};
+      Group g{0, b, c0, std::min<int32_t>(nt, c0 + int32_t(cap)), -1};
       for (int32_t t = g.t_begin; t < g.t_end; ++t) g.work += tile_work(len, t * tile, std::min(tile, len - t * tile));
       groups.push_back(g);
     }
+  };
+  for (int32_t b = 0; b < n;) {
+    if (cu[b + 1] - cu[b] >= tile) {
+      add_sequence(b++);
+      continue;
+    }
+    // the run of short sequences from b that fits one tile
+    int32_t e = b, nonempty = 0, last = b;
+    while (e < n && cu[e + 1] - cu[e] < tile && cu[e + 1] - cu[b] <= tile) {
+      if (cu[e + 1] > cu[e]) {
+        ++nonempty;
+        last = e;
+      }
+      ++e;
+    }
+    if (nonempty == 1) {
+      add_sequence(last);
+    } else if (nonempty > 1) {
+      const int32_t w = int32_t(out.window_starts.size() / kWindowWords);
+      out.window_starts.resize(out.window_starts.size() + kWindowWords, 0);
+      uint64_t* m = &out.window_starts[size_t(w) * kWindowWords];
+      const int32_t rows = cu[e] - cu[b];
+      for (int32_t i = b; i < e; ++i) {
+        const int32_t x = cu[i] - cu[b];
+        if (x < rows) m[x / 64] |= uint64_t(1) << (x % 64);
+      }
+      groups.push_back(Group{rows, b, 0, rows, w});
+    }
+    b = e;
   }
   std::stable_sort(groups.begin(), groups.end(), [](const Group& x, const Group& y) { return x.work > y.work; });
-  std::vector<std::vector<WorkUnit>> lists(kNumXcd);
-  for (auto& l : lists) l.reserve(total / kNumXcd + size_t(cap) + 1);
-  int64_t load[kNumXcd] = {0};
   // within a chunk, the tile with the most work first (causal: the last
   // query tiles of the forward, the first key tiles of the dK/dV pass)
   const bool reverse = d->causal && !keys_major;
-  for (const Group& g : groups) {
-    const int32_t s0 = cu[g.b], len = cu[g.b + 1] - cu[g.b];
-    for (int32_t h = 0; h < H; ++h) {
-      // the least-loaded die takes the chunk
-      int x = 0;
-      for (int i = 1; i < kNumXcd; ++i)
-        if (load[i] < load[x]) x = i;
-      load[x] += g.work;
-      std::vector<WorkUnit>& l = lists[size_t(x)];
-      for (int32_t i = g.t_begin; i < g.t_end; ++i) {
-        const int32_t t = reverse ? g.t_end - 1 - (i - g.t_begin) : i;
-        WorkUnit u{};
-        u.row0 = s0 + t * tile;
-        u.rows = uint16_t(std::min(tile, len - t * tile));
-        u.seq0 = s0;
-        u.seqlen = len;
-        u.head = uint16_t(h);
-        l.push_back(u);
+  // sequence tiles and packed windows run as separate launches: each is
+  // balanced over the dies on its own
+  for (int windows = 0; windows < 2; ++windows) {
+    std::vector<std::vector<WorkUnit>> lists(kNumXcd);
+    for (auto& l : lists) l.reserve(total / kNumXcd + size_t(cap) + 1);
+    int64_t load[kNumXcd] = {0};
+    for (const Group& g : groups) {
+      if ((g.window >= 0) != (windows == 1)) continue;
+      const int32_t s0 = cu[g.b], len = cu[g.b + 1] - cu[g.b];
+      for (int32_t h = 0; h < H; ++h) {
+        // the least-loaded die takes the chunk
+        int x = 0;
+        for (int i = 1; i < kNumXcd; ++i)
+          if (load[i] < load[x]) x = i;
+        load[x] += g.work;
+        std::vector<WorkUnit>& l = lists[size_t(x)];
+        if (g.window >= 0) {
+          WorkUnit u{};
+          u.row0 = s0;
+          u.seq0 = s0;
+          u.seqlen = -g.window - 1;
+          u.rows = uint16_t(g.t_end);
+          u.head = uint16_t(h);
+          l.push_back(u);
+          continue;
+        }
+        for (int32_t i = g.t_begin; i < g.t_end; ++i) {
+          const int32_t t = reverse ? g.t_end - 1 - (i - g.t_begin) : i;
+          WorkUnit u{};
+          u.row0 = s0 + t * tile;
+          u.rows = uint16_t(std::min(tile, len - t * tile));
+          u.seq0 = s0;
+          u.seqlen = len;
+          u.head = uint16_t(h);
+          l.push_back(u);
+        }
       }
     }
+    size_t per = 0;
+    for (const auto& l : lists) per = std::max(per, l.size());
+    const size_t at = out.units.size();
+    out.units.resize(at + per * kNumXcd, WorkUnit{});
+    for (int x = 0; x < kNumXcd; ++x)
+      std::copy(lists[size_t(x)].begin(), lists[size_t(x)].end(), out.units.begin() + ptrdiff_t(at + size_t(x) * per));
+    if (windows == 0) out.n_tiles = out.units.size();
   }
-  size_t per = 0;
-  for (const auto& l : lists) per = std::max(per, l.size());
-  out.assign(per * kNumXcd, WorkUnit{});
-  for (int x = 0; x < kNumXcd; ++x)
-    std::copy(lists[size_t(x)].begin(), lists[size_t(x)].end(), out.begin() + ptrdiff_t(size_t(x) * per));
   return out;
 }
 
@@ -179,17 +237,29 @@ size_t count_units(const dcp_attn_desc* d, int tile) {
   return tiles_per_head(d, tile) * size_t(d->n_heads) * kNumXcd;
 }
 
-// Backward workspace: constant chunks | key-tile list | query-tile list |
-// LSE*log2e [H, T] | Delta [H, T].
+// Bytes reserved for one work list and, after it, its window masks (there
+// are fewer windows than tiles of one head).
+size_t list_bytes(const dcp_attn_desc* d, int tile) {
+  return align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, tile)));
+}
+size_t window_bytes(const dcp_attn_desc* d, int tile) {
+  return align_up(sizeof(uint64_t) * kWindowWords * std::max<size_t>(1, tiles_per_head(d, tile)));
+}
+
+// Backward workspace: constant chunks | key-tile list | its window masks |
+// query-tile list | its window masks | LSE*log2e [H, T] | Delta [H, T].
 struct BwdLayout {
-  size_t units, qunits, lse2, delta, total;
+  size_t units, windows, qunits, qwindows, lse2, delta, total;
 };
 BwdLayout bwd_layout(const dcp_attn_desc* d) {
   const size_t per_row = align_up(size_t(4) * size_t(d->n_heads) * size_t(d->total_tokens));
+  const int kt = bwd_key_tile_rows(d->head_dim), qt = bwd_query_tile_rows(d->head_dim);
   BwdLayout l;
   l.units = kConstBytes;
-  l.qunits = l.units + align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, bwd_key_tile_rows(d->head_dim))));
-  l.lse2 = l.qunits + align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, bwd_query_tile_rows(d->head_dim))));
+  l.windows = l.units + list_bytes(d, kt);
+  l.qunits = l.windows + window_bytes(d, kt);
+  l.qwindows = l.qunits + list_bytes(d, qt);
+  l.lse2 = l.qwindows + window_bytes(d, qt);
   l.delta = l.lse2 + per_row;
   l.total = l.delta + per_row;
   return l;
@@ -198,26 +268,38 @@ BwdLayout bwd_layout(const dcp_attn_desc* d) {
 // The constant block at the head of a workspace -- 16-byte chunks the
 // kernels' direct-to-LDS copies read for pad columns ([0 x 8] and
 // [1, 0 x 7] in bf16) and for rows past a sequence end (fp32 +inf) --
-// and the work lists, each copied to its byte offset in the workspace
-// (one copy per list: the space reserved between them is not touched).
-int upload_head(std::initializer_list<std::pair<size_t, const std::vector<WorkUnit>*>> lists, void* dst,
-                hipStream_t stream) {
+// and each work list with its window masks, copied to their byte offsets
+// in the workspace (one copy per array: the space reserved between them
+// is not touched).
+struct ListAt {
+  size_t units_at, windows_at;
+  const UnitList* list;
+};
+int upload_head(std::initializer_list<ListAt> lists, void* dst, hipStream_t stream) {
   unsigned char head[kConstBytes] = {};
   const uint16_t one = 0x3F80;  // bf16 1.0
   std::memcpy(head + kConstOnes * 2, &one, sizeof one);
   const float inf = std::numeric_limits<float>::infinity();
   std::memcpy(head + kConstInf * 2, &inf, sizeof inf);
+  unsigned char* base = static_cast<unsigned char*>(dst);
   hipError_t e = hipMemcpyAsync(dst, head, sizeof head, hipMemcpyHostToDevice, stream);
-  for (const auto& l : lists)
-    if (e == hipSuccess && !l.second->empty())
-      e = hipMemcpyAsync(static_cast<unsigned char*>(dst) + l.first, l.second->data(),
-                         l.second->size() * sizeof(WorkUnit), hipMemcpyHostToDevice, stream);
+  for (const ListAt& l : lists) {
+    const UnitList& u = *l.list;
+    if (e == hipSuccess && !u.units.empty())
+      e = hipMemcpyAsync(base + l.units_at, u.units.data(), u.units.size() * sizeof(WorkUnit), hipMemcpyHostToDevice,
+                         stream);
+    if (e == hipSuccess && !u.window_starts.empty())
+      e = hipMemcpyAsync(base + l.windows_at, u.window_starts.data(), u.window_starts.size() * sizeof(uint64_t),
+                         hipMemcpyHostToDevice, stream);
+  }
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
   return DCP_OK;
 }
 
+// Forward workspace: constant chunks | tile list | its window masks.
+size_t fwd_windows_at(const dcp_attn_desc* d) { return kConstBytes + list_bytes(d, fwd_tile_rows(d->head_dim)); }
 size_t fwd_workspace_bytes(const dcp_attn_desc* d) {
-  return align_up(kConstBytes + sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, fwd_tile_rows(d->head_dim))));
+  return fwd_windows_at(d) + window_bytes(d, fwd_tile_rows(d->head_dim));
 }
 
 }  // namespace
@@ -270,13 +352,15 @@ extern "C" int dcp_varlen_attn_fwd(const dcp_attn_desc* desc, const void* q, con
     return fail(DCP_ERR_WORKSPACE, "forward workspace needs %zu bytes, got %zu", need, workspace_bytes);
   if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(DCP_ERR_INVALID, "workspace must be 16-byte aligned");
   if ((st = check_device())) return st;
-  const std::vector<WorkUnit> units = build_units(desc, tile, false);
-  if (units.empty()) return DCP_OK;
+  const UnitList units = build_units(desc, tile, false);
+  if (units.units.empty()) return DCP_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = upload_head({{kConstBytes, &units}}, workspace, s))) return st;
+  const size_t windows_at = fwd_windows_at(desc);
+  if ((st = upload_head({{kConstBytes, windows_at, &units}}, workspace, s))) return st;
   char* ws = static_cast<char*>(workspace);
-  FwdArgs a{q, k, v, o, lse, ws, ws + kConstBytes, int(units.size()), desc->n_heads, desc->head_dim,
-            int(desc->total_tokens), desc->scale, desc->causal, s};
+  FwdArgs a{q, k, v, o, lse, ws, ws + kConstBytes, ws + windows_at, int(units.n_tiles),
+            int(units.units.size() - units.n_tiles), desc->n_heads, desc->head_dim, int(desc->total_tokens),
+            desc->scale, desc->causal, s};
   hipError_t e = launch_fwd(a);
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "forward launch: %s", hipGetErrorString(e));
   return DCP_OK;
@@ -298,19 +382,54 @@ extern "C" int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, 
     return fail(DCP_ERR_WORKSPACE, "backward workspace needs %zu bytes, got %zu", l.total, workspace_bytes);
   if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(DCP_ERR_INVALID, "workspace must be 16-byte aligned");
   if ((st = check_device())) return st;
-  const std::vector<WorkUnit> units = build_units(desc, bwd_key_tile_rows(desc->head_dim), true);
-  if (units.empty()) return DCP_OK;
-  const std::vector<WorkUnit> qunits = build_units(desc, bwd_query_tile_rows(desc->head_dim), false);
+  const UnitList units = build_units(desc, bwd_key_tile_rows(desc->head_dim), true);
+  if (units.units.empty()) return DCP_OK;
+  const UnitList qunits = build_units(desc, bwd_query_tile_rows(desc->head_dim), false);
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
-  if ((st = upload_head({{l.units, &units}, {l.qunits, &qunits}}, workspace, s))) return st;
+  if ((st = upload_head({{l.units, l.windows, &units}, {l.qunits, l.qwindows, &qunits}}, workspace, s))) return st;
   BwdArgs a{dout, o, lse, q, k, v, dq, dk, dv, reinterpret_cast<float*>(ws + l.delta),
-            reinterpret_cast<float*>(ws + l.lse2), ws, ws + l.units, int(units.size()), ws + l.qunits,
-            int(qunits.size()),
+            reinterpret_cast<float*>(ws + l.lse2), ws, ws + l.units, ws + l.windows, int(units.n_tiles),
+            int(units.units.size() - units.n_tiles), ws + l.qunits, ws + l.qwindows, int(qunits.n_tiles),
+            int(qunits.units.size() - qunits.n_tiles),
             desc->cu_seqlens_host[desc->n_seqs], desc->n_heads, desc->head_dim, int(desc->total_tokens),
             desc->scale, desc->causal, s};
   hipError_t e = launch_bwd(a);
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "backward launch: %s", hipGetErrorString(e));
+  return DCP_OK;
+}
+
+extern "C" int dcp_work_list(const dcp_attn_desc* desc, int32_t pass, int32_t* units, size_t cap, size_t* n_units,
+                             size_t* n_tiles, uint64_t* window_starts, size_t cap_windows, size_t* n_windows) {
+  clear_error();
+  int st = validate_desc(desc);
+  if (st) return st;
+  if (!n_units || !n_tiles || !n_windows) return fail(DCP_ERR_INVALID, "count outputs are null");
+  int tile = 0;
+  switch (pass) {
+    case 0: tile = fwd_tile_rows(desc->head_dim); break;
+    case 1: tile = bwd_key_tile_rows(desc->head_dim); break;
+    case 2: tile = bwd_query_tile_rows(desc->head_dim); break;
+    default: return fail(DCP_ERR_INVALID, "pass must be 0 (forward), 1 (dK/dV) or 2 (dQ)");
+  }
+  const UnitList l = build_units(desc, tile, pass == 1);
+  const size_t nw = l.window_starts.size() / kWindowWords;
+  if (units && cap < l.units.size()) return fail(DCP_ERR_INVALID, "units holds %zu, need %zu", cap, l.units.size());
+  if (window_starts && cap_windows < nw) return fail(DCP_ERR_INVALID, "window_starts holds %zu, need %zu", cap_windows, nw);
+  *n_units = l.units.size();
+  *n_tiles = l.n_tiles;
+  *n_windows = nw;
+  if (units)
+    for (size_t i = 0; i < l.units.size(); ++i) {
+      const WorkUnit& u = l.units[i];
+      int32_t* o = units + 5 * i;
+      o[0] = u.row0;
+      o[1] = u.seq0;
+      o[2] = u.seqlen;
+      o[3] = u.rows;
+      o[4] = u.head;
+    }
+  if (window_starts && nw) std::memcpy(window_starts, l.window_starts.data(), l.window_starts.size() * sizeof(uint64_t));
   return DCP_OK;
 }
 
