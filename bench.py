@@ -36,7 +36,9 @@ HBM_PEAK_GBS = 8000.0
 # of known size reads), per workload; valid only for the kernel sources
 # whose hash is recorded with them.
 MEASURED_TRAFFIC = {
-    "video_short": {"sources_sha256_16": "e2467e7b21542796", "bytes": (1125737.0 * 2.0 + 691200.5) * 1024},
+    "video_short": {"sources_sha256_16": "58bc4088824769dc", "bytes": (1117887.4 * 2.0 + 691206.8 * 1.0) * 1024},
+    "video2d_temporal": {"sources_sha256_16": "58bc4088824769dc",
+                         "bytes": (1062647.1 * 2.0 + 655361.5 * 1.0) * 1024},
 }
 KERNEL_SOURCES = ("attn_bwd.hip", "attn_common.h", "attn_launch.h")
 
@@ -178,6 +180,33 @@ def cpu_baseline(w, rng_seed: int, budget_s: float = 12.0):
                       f"({w.n_heads} heads, D={w.head_dim}) in {t_total:.1f} s"}
 
 
+def dkdv_bytes(cu, H: int, D: int) -> float:
+    """Algorithmic HBM bytes of the dK/dV pass: Q, K, V, dO read and dK, dV
+    written once (bf16), LSE and Delta read once (fp32), over the rows of
+    the sequences."""
+    rows = int(cu[-1])
+    return 6.0 * rows * H * D * 2 + 2.0 * rows * H * 4
+
+
+def roofline(flop: float, nbytes: float, ms: float, traffic) -> dict:
+    """Roofline of the dK/dV pass: matrix-bound when its arithmetic
+    intensity is above the ridge point (bf16 peak / HBM peak), else
+    HBM-bound (short sequences: intensity grows with the sequence length)."""
+    mfma = flop / nbytes >= BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    out = {"kernel": "attn_bwd_dkdv_kernel", "flop_per_launch": flop, "bytes_per_launch": nbytes,
+           "flop_convention": "8*pairs*H*D (S, dP, dV, dK products)",
+           "bytes_convention": "6*rows*H*D*2 + 2*rows*H*4 (Q, K, V, dO, dK, dV; LSE, Delta)",
+           "traffic": traffic,
+           "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)"}
+    if mfma:
+        a = flop / (ms * 1e-3) / 1e12
+        out.update(bound="mfma", achieved=a, peak=BF16_PEAK_TFLOPS, unit="TFLOP/s", frac=a / BF16_PEAK_TFLOPS)
+    else:
+        a = nbytes / (ms * 1e-3) / 1e9
+        out.update(bound="hbm", achieved=a, peak=HBM_PEAK_GBS, unit="GB/s", frac=a / HBM_PEAK_GBS)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -266,11 +295,7 @@ def main():
                    "flop_convention": "fwd 4*pairs*H*D + bwd 10*pairs*H*D"},
         "kernels": {"fwd_ms": fwd_ms, "fwd_tflops": fwd_tflops, "bwd_dkdv_ms": bwd_ms, "bwd_dkdv_tflops": dkdv_tflops,
                     "bwd_rest_ms": ms - fwd_ms - bwd_ms},
-        "roofline": {"kernel": "attn_bwd_dkdv_kernel", "bound": "mfma", "achieved": dkdv_tflops,
-                     "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": dkdv_tflops / BF16_PEAK_TFLOPS,
-                     "traffic": measured_traffic(args.workload),
-                     "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
-                     "flop_per_launch": flop_dkdv, "flop_convention": "8*pairs*H*D (S, dP, dV, dK products)"},
+        "roofline": roofline(flop_dkdv, dkdv_bytes(cu, H, D), bwd_ms, measured_traffic(args.workload)),
         "padded_baseline": padded,
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(w, args.seed),
     }

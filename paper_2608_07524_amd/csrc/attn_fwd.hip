@@ -348,16 +348,23 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
     // P = exp2(S*scale*log2e - m) as bf16 (B operand of the PV product)
     const float mneg = -m_use;
     bf16x8 pb[2];
-    float lsum = 0.f;
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sc[8 * hh + e], scale_log2, mneg));
-        if (!S::ONES_ROW) lsum += p;
-        pb[hh][e] = __bf16(p);
-      }
-    if (!S::ONES_ROW) l_run += lsum;
+      for (int e = 0; e < 8; ++e) pb[hh][e] = __bf16(__builtin_amdgcn_exp2f(fmaf(sc[8 * hh + e], scale_log2, mneg)));
+    if constexpr (!S::ONES_ROW) {
+      // the row sum over the same bf16 weights the PV product uses, so that
+      // O = sum_j w_j v_j / sum_j w_j is an exact weighted mean of V rows
+      // (pairwise dot products with (1, 1), one accumulator per half)
+      const bf16x2 one = {__bf16(1.f), __bf16(1.f)};
+      float lh[2] = {0.f, 0.f};
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          lh[hh] = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[hh][2 * i], pb[hh][2 * i + 1]}, one, lh[hh], false);
+      l_run += lh[0] + lh[1];
+    }
     if constexpr (MASK) apply_mask(sn, bn);
     pv_product(pb, vcur);
     if (DCP_FWD_SCHED) {

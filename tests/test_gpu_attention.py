@@ -14,7 +14,7 @@ import pytest
 from oracle import attention as A
 from paper_2608_07524_amd import inputs as I
 
-from gpu_util import GRAD_TOL, LSE_TOL, O_TOL, grad_err, max_abs, to_bits, to_device
+from gpu_util import GRAD_TOL, LSE_TOL, O_TOL, grad_err, max_abs, o_excess, to_bits, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -60,12 +60,14 @@ def _run_case(torch, lengths, H, D, causal, scale=None, seed=0):
 def _assert_close(got, ref, n, label):
     ref_o, ref_lse, ref_dq, ref_dk, ref_dv = ref
     eo = max_abs(got["o"][:n], ref_o)
+    xo = o_excess(got["o"][:n], ref_o) if n else 0.0
     el = float(np.max(np.abs(got["lse"][:, :n] - ref_lse))) if n else 0.0
     eq = grad_err(got["dq"][:n], ref_dq) if n else 0.0
     ek = grad_err(got["dk"][:n], ref_dk) if n else 0.0
     ev = grad_err(got["dv"][:n], ref_dv) if n else 0.0
-    print(f"{label}: O {eo:.2e} LSE {el:.2e} dQ {eq:.2e} dK {ek:.2e} dV {ev:.2e}", flush=True)
-    assert eo <= O_TOL and el <= LSE_TOL
+    print(f"{label}: O {eo:.2e} (beyond bf16 rounding {xo:.2e}) LSE {el:.2e} dQ {eq:.2e} dK {ek:.2e} dV {ev:.2e}",
+          flush=True)
+    assert xo <= O_TOL and el <= LSE_TOL
     assert eq <= GRAD_TOL and ek <= GRAD_TOL and ev <= GRAD_TOL
 
 
@@ -91,6 +93,20 @@ def test_many_tiny_sequences(torch):
     lengths = rng.integers(1, 17, 300).tolist()
     got, ref, n = _run_case(torch, lengths, 2, 72, False, seed=3)
     _assert_close(got, ref, n, "300 seqs of 1..16")
+
+
+@pytest.mark.parametrize("D", [64, 72, 128])
+@pytest.mark.parametrize("causal", [False, True])
+def test_packed_windows(torch, D, causal):
+    """Runs of short sequences share one tile (packed windows): sequences
+    that cross 32- and 64-row block edges inside a window, empty ones among
+    them, windows of every size up to a full tile, next to long sequences."""
+    rng = np.random.default_rng(40 + D + causal)
+    lengths = rng.integers(1, 200, 40)
+    lengths[rng.integers(0, 40, 6)] = 0
+    lengths = np.concatenate([lengths, [700], rng.integers(1, 8, 30), [130, 126], [31, 33, 64, 127, 1]]).tolist()
+    got, ref, n = _run_case(torch, lengths, 3, D, causal, seed=D + 1)
+    _assert_close(got, ref, n, f"windows D={D} causal={causal}")
 
 
 def test_single_long_sequence(torch):

@@ -17,7 +17,7 @@ import pytest
 from oracle import attention as A
 from paper_2608_07524_amd import inputs as I
 
-from gpu_util import GRAD_TOL, LSE_TOL, O_TOL, to_bits, to_device
+from gpu_util import BF16_U, GRAD_TOL, LSE_TOL, O_TOL, to_bits, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -71,11 +71,12 @@ def _check_rows(bits, out, w, rng, n_random, label):
     gl = out["lse"][heads, rows]
     gdq = I.bf16_to_f64(out["dq"][rows, heads])
     eo = float(np.max(np.abs(go - ro)))
+    xo = float(np.max(np.abs(go - ro) - BF16_U * np.abs(ro)))  # beyond the bf16 store rounding
     el = float(np.max(np.abs(gl - rl)))
     # dQ relative to the largest reference magnitude over the sampled rows
     edq = float(np.max(np.abs(gdq - rdq)) / np.max(np.abs(rdq)))
     print(f"{label}: {rows.size} sampled rows: O {eo:.2e} LSE {el:.2e} dQ {edq:.2e}", flush=True)
-    assert eo <= O_TOL and el <= LSE_TOL and edq <= GRAD_TOL
+    assert xo <= O_TOL and el <= LSE_TOL and edq <= GRAD_TOL
     return q, k, v, do
 
 

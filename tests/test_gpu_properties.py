@@ -1,6 +1,8 @@
-"""GPU properties that hold exactly: run-to-run bitwise determinism of every
-output, bitwise invariance of a sequence's outputs to its position in the
-pack, and the cost profiler feeding the planner."""
+"""GPU properties: run-to-run bitwise determinism of every output, bitwise
+invariance of a sequence's outputs to its position in the pack (sequences
+that run in tiles of their own), the same within the parity bounds for
+short sequences sharing a packed window, and the cost profiler feeding the
+planner."""
 
 import math
 
@@ -64,6 +66,32 @@ def test_position_in_pack_invariance(torch, causal):
             assert np.array_equal(x, y[:, sl])
         else:
             assert np.array_equal(x, y[sl])
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_packed_window_neighbours(torch, causal):
+    """A short sequence shares a tile with its short neighbours (a packed
+    window): its outputs match those it gets alone within the parity bounds,
+    whatever its neighbours hold (each row is masked to its own sequence)."""
+    from gpu_util import BF16_U, GRAD_TOL, LSE_TOL, O_TOL
+    rng = np.random.default_rng(9)
+    H, D = 2, 72
+    target = I.tensors(rng, 45, H, D)
+    solo = _outputs(torch, target, [0, 45], 0.1, causal)
+    for left_len, right_len in [(19, 100), (70, 3), (1, 150)]:
+        left = I.tensors(rng, left_len, H, D)
+        right = I.tensors(rng, right_len, H, D)
+        bits = [np.concatenate([l, t, r]) for l, t, r in zip(left, target, right)]
+        cu = [0, left_len, left_len + 45, left_len + 45 + right_len]
+        packed = _outputs(torch, bits, cu, 0.1, causal)
+        sl = slice(left_len, left_len + 45)
+        x = [I.bf16_to_f64(a) for a in (solo[0], packed[0][sl])]
+        # each within the O bound of the exact result (bf16 store rounding added)
+        assert np.max(np.abs(x[0] - x[1]) - 2 * BF16_U * np.abs(x[0])) <= 2 * O_TOL
+        assert np.max(np.abs(solo[1] - packed[1][:, sl])) <= LSE_TOL
+        for i in (2, 3, 4):
+            a, b = I.bf16_to_f64(solo[i]), I.bf16_to_f64(packed[i][sl])
+            assert np.max(np.abs(a - b)) <= GRAD_TOL * np.max(np.abs(a))
 
 
 def test_profile_cost_rows(torch):
