@@ -73,8 +73,14 @@ constexpr int kSchedMfma = 0x008;
 constexpr int kSchedValu = 0x002;
 constexpr int kSchedDsRead = 0x100;
 
+#ifdef DCP_FWD_WPE
+#define DCP_FWD_OCCUPANCY __attribute__((amdgpu_waves_per_eu(DCP_FWD_WPE)))
+#else
+#define DCP_FWD_OCCUPANCY
+#endif
+
 template <int D, int NW, bool CAUSAL, bool PACKED>
-__global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restrict__ q,
+__global__ __launch_bounds__(64 * NW) DCP_FWD_OCCUPANCY void attn_fwd_kernel(const __bf16* __restrict__ q,
                                                            const __bf16* __restrict__ k,
                                                            const __bf16* __restrict__ v, __bf16* __restrict__ o,
                                                            float* __restrict__ lse,
