@@ -291,6 +291,67 @@ int dcp_plan(const int64_t* seq_lens, int32_t n_seqs, const int32_t* batch_offse
              const dcp_cost_table* table, int64_t hbm_budget_bytes, const dcp_plan_opts* opts,
              dcp_plan_out* out);
 
+/* ------------------------------------------------------------------------ */
+/* Schedule replay: DCP against bucket parallelism (Secs. 2.3-2.4, 4.1-4.2)   */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Replay options:
+ *   n_devices     W, the devices of the data-parallel job (>= 1).
+ *   bucket_sp     the fixed sequence-parallel size of the bucket-parallel
+ *                 baseline; 0 picks the smallest candidate p (dividing
+ *                 n_heads unless DCP_PLAN_FLAG_NO_HEAD_FILTER) at which
+ *                 every batch of the stream fits at micro-batch 1.
+ *   iter_sync_ns  time of the once-per-iteration gradient synchronisation
+ *                 (Sec. 2.4), added to every iteration of both schedules.
+ */
+typedef struct {
+  int32_t n_devices;
+  int32_t bucket_sp;
+  int64_t iter_sync_ns;
+} dcp_sim_opts;
+
+/*
+ * Totals over the replayed iterations.  Throughput (Eq. (1), tokens per
+ * second) = tokens / time_ns * 1e9; the imbalance ratio of Sec. 4.2 (the
+ * share of device time spent waiting for other devices) =
+ * 1 - busy_device_ns / (n_devices * makespan_ns).
+ *   iterations      iterations formed from the stream.
+ *   makespan_ns     sum of the iterations' compute spans, max_i g_i*T_i.
+ *   time_ns         makespan_ns + iterations * iter_sync_ns.
+ *   busy_device_ns  sum of p_i * g_i * T_i over every batch.
+ *   tokens          sum of g_i * b_i * S_i (S_i: tokens of batch i).
+ *   bucket_sp       the baseline's sequence-parallel size (0 for DCP).
+ */
+typedef struct {
+  int64_t iterations;
+  int64_t makespan_ns;
+  int64_t time_ns;
+  int64_t busy_device_ns;
+  int64_t tokens;
+  int32_t bucket_sp;
+} dcp_sim_result;
+
+/*
+ * Replays a stream of batches (same arguments and validation as dcp_plan)
+ * on W devices under two schedules.
+ * DCP: each batch takes the planner's (p_i, b_i, r_i, T_i) (opts->mode
+ * selects DCP-intra or DCP-inter); batches join the current iteration in
+ * stream order while sum_i p_i <= W (the constraint of Eq. (1); devices left
+ * over wait out the iteration), and the iteration's accumulation steps g_i
+ * follow Eq. (3) within the bounds of Appendix C.
+ * Bucket parallelism (the baseline of Sec. 4.1, the static batch sizing of
+ * Sec. 2.4): one fixed p, floor(W/p) batches per iteration in stream order,
+ * full recomputation, g_i = 1, and per batch the largest b <= b_max whose
+ * step time does not exceed the stream's slowest batch at b = 1 and whose
+ * memory fits.
+ * Integer arithmetic throughout; results are bit-exact.  Errors as for
+ * dcp_plan, plus DCP_ERR_INVALID when a batch needs more than W devices.
+ */
+int dcp_simulate(const int64_t* seq_lens, int32_t n_seqs, const int32_t* batch_offsets, int32_t n_batches,
+                 const dcp_cost_table* table, int64_t hbm_budget_bytes, const dcp_plan_opts* opts,
+                 const dcp_sim_opts* sim, dcp_sim_result* dcp_out, dcp_sim_result* bucket_out);
+
 #ifdef __cplusplus
 }
 #endif

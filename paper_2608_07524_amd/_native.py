@@ -74,6 +74,15 @@ class PlanOutC(C.Structure):
                 ("mem_bytes", C.POINTER(C.c_int64)), ("idle_ns", C.c_int64), ("makespan_ns", C.c_int64)]
 
 
+class SimOptsC(C.Structure):
+    _fields_ = [("n_devices", C.c_int32), ("bucket_sp", C.c_int32), ("iter_sync_ns", C.c_int64)]
+
+
+class SimResultC(C.Structure):
+    _fields_ = [("iterations", C.c_int64), ("makespan_ns", C.c_int64), ("time_ns", C.c_int64),
+                ("busy_device_ns", C.c_int64), ("tokens", C.c_int64), ("bucket_sp", C.c_int32)]
+
+
 _lib = None
 
 
@@ -102,6 +111,9 @@ def load() -> C.CDLL:
         "dcp_plan_opts_default": ([C.POINTER(PlanOptsC)], None),
         "dcp_plan": ([C.POINTER(C.c_int64), C.c_int32, C.POINTER(C.c_int32), C.c_int32, C.POINTER(CostTableC),
                       C.c_int64, C.POINTER(PlanOptsC), C.POINTER(PlanOutC)], C.c_int),
+        "dcp_simulate": ([C.POINTER(C.c_int64), C.c_int32, C.POINTER(C.c_int32), C.c_int32, C.POINTER(CostTableC),
+                          C.c_int64, C.POINTER(PlanOptsC), C.POINTER(SimOptsC), C.POINTER(SimResultC),
+                          C.POINTER(SimResultC)], C.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -322,28 +334,34 @@ def default_plan_opts() -> dict:
                 g_min=o.g_min, g_max=o.g_max, mode=o.mode, flags=o.flags)
 
 
-def plan(seq_lens: Sequence[int], rows: Sequence, n_layers: int, T_C_ns: int, M_C_bytes: int, hbm_budget: int,
-         batch_offsets: Optional[Sequence[int]] = None, n_batches: Optional[int] = None, **opts) -> Plan:
-    """Plan one iteration (see dcp_plan).  ``rows``: (seq_len, t_f, t_b, m, m_inp)
-    tuples or CostRow objects; ``opts`` override dcp_plan_opts_default."""
-    lib = load()
+def _plan_opts(lib, opts):
+    """dcp_plan_opts from the defaults with ``opts`` overrides; returns the
+    struct and the arrays it points to (kept alive by the caller)."""
     o = PlanOptsC()
     lib.dcp_plan_opts_default(C.byref(o))
-    sp = None
+    keep = []
     for key, val in opts.items():
         if key == "sp_cands":
             sp = np.ascontiguousarray(np.asarray(val, dtype=np.int32))
+            keep.append(sp)
             o.sp_cands = sp.ctypes.data_as(C.POINTER(C.c_int32))
             o.n_sp = int(sp.size)
         elif hasattr(o, key):
             setattr(o, key, int(val))
         else:
             raise TypeError(f"unknown planner option {key}")
+    return o, keep
+
+
+def _cost_table(rows, n_layers, T_C_ns, M_C_bytes):
     crow = (CostRow * len(rows))()
     for i, r in enumerate(rows):
         vals = (r.seq_len, r.t_f_ns, r.t_b_ns, r.m_bytes, r.m_inp_bytes) if hasattr(r, "seq_len") else tuple(r)
         crow[i] = CostRow(*[int(x) for x in vals])
-    table = CostTableC(crow, len(rows), int(n_layers), int(T_C_ns), int(M_C_bytes))
+    return CostTableC(crow, len(rows), int(n_layers), int(T_C_ns), int(M_C_bytes)), crow
+
+
+def _batches(seq_lens, batch_offsets, n_batches):
     lens = np.ascontiguousarray(np.asarray(seq_lens, dtype=np.int64))
     offs = None
     if batch_offsets is not None:
@@ -351,6 +369,17 @@ def plan(seq_lens: Sequence[int], rows: Sequence, n_layers: int, T_C_ns: int, M_
         nb = int(offs.size - 1) if n_batches is None else int(n_batches)
     else:
         nb = int(lens.size) if n_batches is None else int(n_batches)
+    return lens, offs, nb
+
+
+def plan(seq_lens: Sequence[int], rows: Sequence, n_layers: int, T_C_ns: int, M_C_bytes: int, hbm_budget: int,
+         batch_offsets: Optional[Sequence[int]] = None, n_batches: Optional[int] = None, **opts) -> Plan:
+    """Plan one iteration (see dcp_plan).  ``rows``: (seq_len, t_f, t_b, m, m_inp)
+    tuples or CostRow objects; ``opts`` override dcp_plan_opts_default."""
+    lib = load()
+    o, _keep = _plan_opts(lib, opts)
+    table, _rows = _cost_table(rows, n_layers, T_C_ns, M_C_bytes)
+    lens, offs, nb = _batches(seq_lens, batch_offsets, n_batches)
     nb_alloc = max(nb, 1)
     i32 = lambda: (C.c_int32 * nb_alloc)()
     i64 = lambda: (C.c_int64 * nb_alloc)()
@@ -364,3 +393,22 @@ def plan(seq_lens: Sequence[int], rows: Sequence, n_layers: int, T_C_ns: int, M_
     L = int(n_layers)
     return Plan(list(sp_o[:nb]), list(mb_o[:nb]), list(ga_o[:nb]), list(rl_o[:nb]), list(fl_o[:nb * L]),
                 list(st_o[:nb]), list(mem_o[:nb]), out.idle_ns, out.makespan_ns)
+
+
+def simulate(seq_lens: Sequence[int], rows: Sequence, n_layers: int, T_C_ns: int, M_C_bytes: int, hbm_budget: int,
+             n_devices: int, bucket_sp: int = 0, iter_sync_ns: int = 0,
+             batch_offsets: Optional[Sequence[int]] = None, n_batches: Optional[int] = None, **opts):
+    """Replay a stream of batches under DCP and under bucket parallelism (see
+    dcp_simulate).  Returns two dicts of totals (iterations, makespan_ns,
+    time_ns, busy_device_ns, tokens, bucket_sp), DCP's first."""
+    lib = load()
+    o, _keep = _plan_opts(lib, opts)
+    table, _rows = _cost_table(rows, n_layers, T_C_ns, M_C_bytes)
+    lens, offs, nb = _batches(seq_lens, batch_offsets, n_batches)
+    sim = SimOptsC(int(n_devices), int(bucket_sp), int(iter_sync_ns))
+    a, b = SimResultC(), SimResultC()
+    _check(lib.dcp_simulate(lens.ctypes.data_as(C.POINTER(C.c_int64)), int(lens.size),
+                            None if offs is None else offs.ctypes.data_as(C.POINTER(C.c_int32)), nb,
+                            C.byref(table), int(hbm_budget), C.byref(o), C.byref(sim), C.byref(a), C.byref(b)))
+    as_dict = lambda r: {k: int(getattr(r, k)) for k, _ in SimResultC._fields_}
+    return as_dict(a), as_dict(b)

@@ -120,6 +120,35 @@ const dcp_cost_row* row_for(const dcp_cost_table* t, int64_t s) {
   return it == hi ? nullptr : it;
 }
 
+// Per-layer costs of b copies of a batch on p devices: the Ulysses
+// all-to-all term c, then t_f, t_b, m, m_inp and base = L*m_inp + M_C
+// (Eq. (6) with every layer recomputed).
+struct LayerCost {
+  int64_t t_f, t_b, m, m_inp, base;
+};
+LayerCost layer_cost(const Unit& u, const dcp_cost_table* t, const dcp_plan_opts& o, int64_t p, int64_t b) {
+  const int64_t L = t->n_layers;
+  int64_t c = 0;
+  if (p != 1) {
+    int64_t vol = chk(i128(chk(i128(chk(i128(b) * u.tokens)) * o.hidden)) * 2);
+    int64_t per_link = chk(i128(chk(i128(p) * p)) * o.link_bytes_per_ns);
+    c = chk(i128(4) * chk(i128(o.a2a_alpha_ns) + ceil_div(vol, per_link)));
+  }
+  LayerCost k;
+  k.t_f = chk(i128(ceil_div(chk(i128(b) * u.t_f), p)) + c);
+  k.t_b = chk(i128(ceil_div(chk(i128(b) * u.t_b), p)) + c);
+  k.m = ceil_div(chk(i128(b) * u.m), p);
+  k.m_inp = ceil_div(chk(i128(b) * u.m_inp), p);
+  k.base = chk(i128(chk(i128(L) * k.m_inp)) + t->M_C_bytes);
+  return k;
+}
+
+// Eqs. (4)-(5): T = L*(t_f + t_b) + r*t_f + T_C.
+int64_t step_time(const LayerCost& k, int64_t r, const dcp_cost_table* t) {
+  const int64_t L = t->n_layers;
+  return chk(i128(chk(i128(chk(i128(L) * chk(i128(k.t_f) + k.t_b))) + chk(i128(r) * k.t_f))) + t->T_C_ns);
+}
+
 // Returns DCP_OK and fills `best`, or an error status.
 int choose(const Unit& u, const dcp_cost_table* t, int64_t budget, const dcp_plan_opts& o, int32_t batch,
            Choice* best_out) {
@@ -130,17 +159,8 @@ int choose(const Unit& u, const dcp_cost_table* t, int64_t budget, const dcp_pla
     const int64_t p = o.sp_cands[pi];
     if (!(o.flags & DCP_PLAN_FLAG_NO_HEAD_FILTER) && (o.n_heads % p) != 0) continue;
     for (int64_t b = 1; b <= o.b_max; ++b) {
-      int64_t c = 0;
-      if (p != 1) {
-        int64_t vol = chk(i128(chk(i128(chk(i128(b) * u.tokens)) * o.hidden)) * 2);
-        int64_t per_link = chk(i128(chk(i128(p) * p)) * o.link_bytes_per_ns);
-        c = chk(i128(4) * chk(i128(o.a2a_alpha_ns) + ceil_div(vol, per_link)));
-      }
-      const int64_t t_f = chk(i128(ceil_div(chk(i128(b) * u.t_f), p)) + c);
-      const int64_t t_b = chk(i128(ceil_div(chk(i128(b) * u.t_b), p)) + c);
-      const int64_t m = ceil_div(chk(i128(b) * u.m), p);
-      const int64_t m_inp = ceil_div(chk(i128(b) * u.m_inp), p);
-      const int64_t base = chk(i128(chk(i128(L) * m_inp)) + t->M_C_bytes);
+      const LayerCost k = layer_cost(u, t, o, p, b);
+      const int64_t m = k.m, base = k.base;
       if (base > budget) continue;
       int64_t r;
       if (o.mode == DCP_PLAN_INTER) {
@@ -149,8 +169,7 @@ int choose(const Unit& u, const dcp_cost_table* t, int64_t budget, const dcp_pla
         const int64_t kept = (m == 0) ? L : std::min<int64_t>(L, (budget - base) / m);
         r = L - kept;
       }
-      const int64_t T = chk(i128(chk(i128(chk(i128(L) * chk(i128(t_f) + t_b))) + chk(i128(r) * t_f))) +
-                            t->T_C_ns);
+      const int64_t T = step_time(k, r, t);
       bool better;
       if (!have) {
         better = true;
@@ -172,6 +191,31 @@ int choose(const Unit& u, const dcp_cost_table* t, int64_t budget, const dcp_pla
   }
   if (!have) return dcp::fail(DCP_ERR_INFEASIBLE, "no feasible configuration for batch %d", batch);
   *best_out = best;
+  return DCP_OK;
+}
+
+// Per-batch sums of the table rows of its sequences (each sequence takes the
+// row with the smallest length >= its own).
+int batch_units(const int64_t* seq_lens, const int32_t* batch_offsets, int32_t n_batches, const dcp_cost_table* table,
+                std::vector<Unit>* out) {
+  std::vector<Unit>& units = *out;
+  units.assign(static_cast<size_t>(n_batches), Unit{});
+  for (int32_t i = 0; i < n_batches; ++i) {
+    const int32_t lo = batch_offsets ? batch_offsets[i] : i;
+    const int32_t hi = batch_offsets ? batch_offsets[i + 1] : i + 1;
+    Unit& u = units[size_t(i)];
+    for (int32_t s = lo; s < hi; ++s) {
+      const dcp_cost_row* r = row_for(table, seq_lens[s]);
+      if (!r)
+        return dcp::fail(DCP_ERR_TABLE, "sequence length %lld exceeds the cost table",
+                         static_cast<long long>(seq_lens[s]));
+      u.tokens = chk(i128(u.tokens) + seq_lens[s]);
+      u.t_f = chk(i128(u.t_f) + r->t_f_ns);
+      u.t_b = chk(i128(u.t_b) + r->t_b_ns);
+      u.m = chk(i128(u.m) + r->m_bytes);
+      u.m_inp = chk(i128(u.m_inp) + r->m_inp_bytes);
+    }
+  }
   return DCP_OK;
 }
 
@@ -237,23 +281,9 @@ extern "C" int dcp_plan(const int64_t* seq_lens, int32_t n_seqs, const int32_t* 
     int st = validate(seq_lens, n_seqs, batch_offsets, n_batches, table, hbm_budget_bytes, o);
     if (st != DCP_OK) return st;
 
-    std::vector<Unit> units(static_cast<size_t>(n_batches));
-    for (int32_t i = 0; i < n_batches; ++i) {
-      const int32_t lo = batch_offsets ? batch_offsets[i] : i;
-      const int32_t hi = batch_offsets ? batch_offsets[i + 1] : i + 1;
-      Unit& u = units[size_t(i)];
-      for (int32_t s = lo; s < hi; ++s) {
-        const dcp_cost_row* r = row_for(table, seq_lens[s]);
-        if (!r)
-          return dcp::fail(DCP_ERR_TABLE, "sequence length %lld exceeds the cost table",
-                           static_cast<long long>(seq_lens[s]));
-        u.tokens = chk(i128(u.tokens) + seq_lens[s]);
-        u.t_f = chk(i128(u.t_f) + r->t_f_ns);
-        u.t_b = chk(i128(u.t_b) + r->t_b_ns);
-        u.m = chk(i128(u.m) + r->m_bytes);
-        u.m_inp = chk(i128(u.m_inp) + r->m_inp_bytes);
-      }
-    }
+    std::vector<Unit> units;
+    st = batch_units(seq_lens, batch_offsets, n_batches, table, &units);
+    if (st != DCP_OK) return st;
     std::vector<Choice> ch(static_cast<size_t>(n_batches));
     std::vector<int64_t> T(static_cast<size_t>(n_batches));
     for (int32_t i = 0; i < n_batches; ++i) {
@@ -288,5 +318,154 @@ extern "C" int dcp_plan(const int64_t* seq_lens, int32_t n_seqs, const int32_t* 
     return dcp::fail(DCP_ERR_INVALID, "int64 overflow in planner arithmetic");
   } catch (...) {
     return dcp::fail(DCP_ERR_INVALID, "planner failed (out of host memory)");
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Schedule replay: DCP against bucket parallelism over a stream of batches
+// on W devices (the comparison of Sec. 4.2: throughput, Eq. (1), and the
+// imbalance ratio, the share of device time spent waiting).
+//
+// DCP: every batch takes the planner's (p_i, b_i, r_i, T_i); batches join
+// the current iteration in stream order while sum_i p_i <= W (Eq. (1)'s
+// constraint; devices left over wait out the iteration); the iteration's
+// accumulation steps g_i follow Eq. (3) with the bounds of Appendix C.
+// Bucket parallelism (Sec. 4.1 baseline, Sec. 2.4): one fixed p for every
+// batch, floor(W/p) batches per iteration in stream order, no accumulation,
+// full recomputation, and a static batch size per batch -- the largest b
+// whose step time does not exceed that of the slowest batch of the stream at
+// b = 1 (long batches stay at 1, short ones grow), within memory.
+// Per iteration: makespan = max_i g_i*T_i, busy device time sum_i
+// p_i*g_i*T_i, tokens sum_i g_i*b_i*S_i, time = makespan + sync.
+
+namespace {
+
+int sim_dcp(const std::vector<Unit>& units, const dcp_cost_table* t, int64_t budget, const dcp_plan_opts& o,
+            int64_t W, int64_t sync, dcp_sim_result* res) {
+  const size_t n = units.size();
+  std::vector<Choice> ch(n);
+  for (size_t i = 0; i < n; ++i) {
+    int st = choose(units[i], t, budget, o, int32_t(i), &ch[i]);
+    if (st != DCP_OK) return st;
+    if (ch[i].p > W) return dcp::fail(DCP_ERR_INVALID, "batch %zu needs %d devices, more than W", i, ch[i].p);
+    if (ch[i].T == 0) return dcp::fail(DCP_ERR_TABLE, "a batch has zero step time; the cost table is empty of cost");
+  }
+  *res = dcp_sim_result{};
+  size_t i = 0;
+  while (i < n) {
+    size_t j = i;
+    int64_t used = 0;
+    while (j < n && used + ch[j].p <= W) used += ch[j++].p;
+    std::vector<int64_t> T(j - i), g;
+    for (size_t k = i; k < j; ++k) T[k - i] = ch[k].T;
+    int64_t idle = 0, span = 0;
+    int st = accumulate(T, o.g_min, o.g_max, &g, &idle, &span);
+    if (st != DCP_OK) return st;
+    i128 busy = 0, tokens = 0;
+    for (size_t k = i; k < j; ++k) {
+      busy += i128(ch[k].p) * g[k - i] * ch[k].T;
+      tokens += i128(g[k - i]) * ch[k].b * units[k].tokens;
+    }
+    res->iterations += 1;
+    res->makespan_ns = chk(i128(res->makespan_ns) + span);
+    res->time_ns = chk(i128(res->time_ns) + span + sync);
+    res->busy_device_ns = chk(i128(res->busy_device_ns) + busy);
+    res->tokens = chk(i128(res->tokens) + tokens);
+    i = j;
+  }
+  return DCP_OK;
+}
+
+int sim_bucket(const std::vector<Unit>& units, const dcp_cost_table* t, int64_t budget, const dcp_plan_opts& o,
+               int64_t W, int64_t sync, int32_t p_req, dcp_sim_result* res) {
+  const int64_t L = t->n_layers;
+  const size_t n = units.size();
+  auto fits_at_one = [&](int64_t p) {
+    for (const Unit& u : units)
+      if (layer_cost(u, t, o, p, 1).base > budget) return false;
+    return true;
+  };
+  int64_t p = p_req;
+  if (p == 0) {
+    for (int32_t pi = 0; pi < o.n_sp && p == 0; ++pi) {
+      const int64_t c = o.sp_cands[pi];
+      if (c > W) break;
+      if (!(o.flags & DCP_PLAN_FLAG_NO_HEAD_FILTER) && (o.n_heads % c) != 0) continue;
+      if (fits_at_one(c)) p = c;
+    }
+    if (p == 0) return dcp::fail(DCP_ERR_INFEASIBLE, "no sequence-parallel size fits every batch at micro-batch 1");
+  } else {
+    if (p > W) return dcp::fail(DCP_ERR_INVALID, "bucket sequence-parallel size exceeds W");
+    if (!fits_at_one(p)) return dcp::fail(DCP_ERR_INFEASIBLE, "a batch does not fit at the bucket sequence-parallel size");
+  }
+  int64_t target = 0;
+  for (const Unit& u : units) target = std::max(target, step_time(layer_cost(u, t, o, p, 1), L, t));
+  if (target == 0) return dcp::fail(DCP_ERR_TABLE, "a batch has zero step time; the cost table is empty of cost");
+  std::vector<int64_t> b(n), T(n);
+  for (size_t i = 0; i < n; ++i) {
+    b[i] = 1;
+    T[i] = step_time(layer_cost(units[i], t, o, p, 1), L, t);
+    for (int64_t bb = 2; bb <= o.b_max; ++bb) {
+      const LayerCost k = layer_cost(units[i], t, o, p, bb);
+      const int64_t Tb = step_time(k, L, t);
+      if (k.base > budget || Tb > target) break;  // both grow with b
+      b[i] = bb;
+      T[i] = Tb;
+    }
+  }
+  *res = dcp_sim_result{};
+  res->bucket_sp = int32_t(p);
+  const size_t per = size_t(W / p);
+  for (size_t i = 0; i < n; i += per) {
+    const size_t j = std::min(n, i + per);
+    int64_t span = 0;
+    i128 busy = 0, tokens = 0;
+    for (size_t k = i; k < j; ++k) {
+      span = std::max(span, T[k]);
+      busy += i128(p) * T[k];
+      tokens += i128(b[k]) * units[k].tokens;
+    }
+    res->iterations += 1;
+    res->makespan_ns = chk(i128(res->makespan_ns) + span);
+    res->time_ns = chk(i128(res->time_ns) + span + sync);
+    res->busy_device_ns = chk(i128(res->busy_device_ns) + busy);
+    res->tokens = chk(i128(res->tokens) + tokens);
+  }
+  return DCP_OK;
+}
+
+}  // namespace
+
+extern "C" int dcp_simulate(const int64_t* seq_lens, int32_t n_seqs, const int32_t* batch_offsets, int32_t n_batches,
+                            const dcp_cost_table* table, int64_t hbm_budget_bytes, const dcp_plan_opts* opts_in,
+                            const dcp_sim_opts* sim, dcp_sim_result* dcp_out, dcp_sim_result* bucket_out) {
+  dcp::clear_error();
+  try {
+    dcp_plan_opts o;
+    if (opts_in) {
+      o = *opts_in;
+    } else {
+      dcp_plan_opts_default(&o);
+    }
+    if (!sim || !dcp_out || !bucket_out) return dcp::fail(DCP_ERR_INVALID, "simulation options and results must not be null");
+    if (sim->n_devices < 1 || sim->bucket_sp < 0 || sim->iter_sync_ns < 0)
+      return dcp::fail(DCP_ERR_INVALID, "need n_devices >= 1, bucket_sp >= 0 and iter_sync_ns >= 0");
+    int st = validate(seq_lens, n_seqs, batch_offsets, n_batches, table, hbm_budget_bytes, o);
+    if (st != DCP_OK) return st;
+    std::vector<Unit> units;
+    st = batch_units(seq_lens, batch_offsets, n_batches, table, &units);
+    if (st != DCP_OK) return st;
+    dcp_sim_result a{}, b{};
+    st = sim_dcp(units, table, hbm_budget_bytes, o, sim->n_devices, sim->iter_sync_ns, &a);
+    if (st != DCP_OK) return st;
+    st = sim_bucket(units, table, hbm_budget_bytes, o, sim->n_devices, sim->iter_sync_ns, sim->bucket_sp, &b);
+    if (st != DCP_OK) return st;
+    *dcp_out = a;
+    *bucket_out = b;
+    return DCP_OK;
+  } catch (const Overflow&) {
+    return dcp::fail(DCP_ERR_INVALID, "int64 overflow in simulation arithmetic");
+  } catch (...) {
+    return dcp::fail(DCP_ERR_INVALID, "simulation failed (out of host memory)");
   }
 }
