@@ -292,6 +292,66 @@ int dcp_plan(const int64_t* seq_lens, int32_t n_seqs, const int32_t* batch_offse
              dcp_plan_out* out);
 
 /* ------------------------------------------------------------------------ */
+/* Transformer layer around the attention (the unit of Secs. 3.4-3.5)        */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * One pre-norm transformer layer over a packed batch: the unit whose
+ * forward time t_f, backward time t_b and stashed activations m the
+ * profiling of Sec. 3.5 measures, and whose forward runs again in the
+ * backward when the layer is recomputed (Eqs. (4)-(6)).
+ *   y1 = RMSNorm(x; norm1), q = y1 Wq, k = y1 Wk, v = y1 Wv,
+ *   o = attention(q, k, v) (dcp_varlen_attn_fwd on `attn`),
+ *   h = x + o Wo, y2 = RMSNorm(h; norm2), a = GELU(y2 Wup) (tanh form),
+ *   out = h + a Wdown.
+ * RMSNorm(z; g) = z * g / sqrt(mean(z^2) + eps) per row.  hidden = H*D of
+ * `attn`, at most 4096 (DCP_ERR_UNSUPPORTED beyond); every row of x is a
+ * token of some sequence (cu_seqlens[n] must equal total_tokens).  GEMMs run in rocBLAS (bf16 in, fp32 accumulation)
+ * with their scratch taken from the caller's workspace; the rocBLAS handle
+ * (one per thread and device, kept until the thread ends) is the only
+ * device memory the library itself holds.
+ */
+typedef struct {
+  const dcp_attn_desc* attn;
+  float eps; /* RMSNorm epsilon, finite and >= 0 */
+} dcp_layer_desc;
+
+/* bf16 device weights, row-major [in, out]: wq, wk, wv, wo [hidden, hidden],
+ * w_up [hidden, 4*hidden], w_down [4*hidden, hidden]; norm1, norm2 [hidden]. */
+typedef struct {
+  const void *norm1, *wq, *wk, *wv, *wo, *norm2, *w_up, *w_down;
+} dcp_layer_weights;
+
+/* fp32 device gradients of the same shapes; the backward adds into them. */
+typedef struct {
+  float *norm1, *wq, *wk, *wv, *wo, *norm2, *w_up, *w_down;
+} dcp_layer_grads;
+
+/* Bytes of the activation stash (kept from forward to backward when the
+ * layer is not recomputed) and of the forward and backward workspaces
+ * (256-byte aligned device memory).  Any output may be NULL. */
+int dcp_layer_sizes(const dcp_layer_desc* desc, size_t* stash_bytes, size_t* fwd_workspace_bytes,
+                    size_t* bwd_workspace_bytes);
+
+/*
+ * Forward: out = layer(x), x and out bf16 [T, hidden].  With a stash
+ * (device, stash_bytes, 256-byte aligned) every activation the backward
+ * needs is kept there; with stash = NULL nothing is kept (the layer will be
+ * recomputed).  Enqueued on `stream`.
+ */
+int dcp_layer_fwd(const dcp_layer_desc* desc, const dcp_layer_weights* w, const void* x, void* out, void* stash,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Backward of <dout, out>: dx (bf16 [T, hidden]) and, added into `grads`,
+ * the weight gradients.  `x` is the forward's input.  `stash` is the
+ * forward's stash, or NULL when the forward kept none: the forward is then
+ * run again first, into the workspace (recomputation).
+ */
+int dcp_layer_bwd(const dcp_layer_desc* desc, const dcp_layer_weights* w, const void* x, const void* dout, void* dx,
+                  const dcp_layer_grads* grads, void* stash, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Schedule replay: DCP against bucket parallelism (Secs. 2.3-2.4, 4.1-4.2)   */
 /* ------------------------------------------------------------------------ */
 

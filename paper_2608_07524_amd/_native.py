@@ -83,6 +83,16 @@ class SimResultC(C.Structure):
                 ("busy_device_ns", C.c_int64), ("tokens", C.c_int64), ("bucket_sp", C.c_int32)]
 
 
+class LayerDescC(C.Structure):
+    _fields_ = [("attn", C.POINTER(AttnDesc)), ("eps", C.c_float)]
+
+
+class LayerWeightsC(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("norm1", "wq", "wk", "wv", "wo", "norm2", "w_up", "w_down")]
+
+
+LAYER_PARAMS = ("norm1", "wq", "wk", "wv", "wo", "norm2", "w_up", "w_down")
+
 _lib = None
 
 
@@ -111,6 +121,10 @@ def load() -> C.CDLL:
         "dcp_plan_opts_default": ([C.POINTER(PlanOptsC)], None),
         "dcp_plan": ([C.POINTER(C.c_int64), C.c_int32, C.POINTER(C.c_int32), C.c_int32, C.POINTER(CostTableC),
                       C.c_int64, C.POINTER(PlanOptsC), C.POINTER(PlanOutC)], C.c_int),
+        "dcp_layer_sizes": ([C.POINTER(LayerDescC), C.POINTER(sz), C.POINTER(sz), C.POINTER(sz)], C.c_int),
+        "dcp_layer_fwd": ([C.POINTER(LayerDescC), C.POINTER(LayerWeightsC), vp, vp, vp, vp, sz, vp], C.c_int),
+        "dcp_layer_bwd": ([C.POINTER(LayerDescC), C.POINTER(LayerWeightsC), vp, vp, vp, C.POINTER(LayerWeightsC), vp,
+                           vp, sz, vp], C.c_int),
         "dcp_simulate": ([C.POINTER(C.c_int64), C.c_int32, C.POINTER(C.c_int32), C.c_int32, C.POINTER(CostTableC),
                           C.c_int64, C.POINTER(PlanOptsC), C.POINTER(SimOptsC), C.POINTER(SimResultC),
                           C.POINTER(SimResultC)], C.c_int),
@@ -412,3 +426,63 @@ def simulate(seq_lens: Sequence[int], rows: Sequence, n_layers: int, T_C_ns: int
                             C.byref(table), int(hbm_budget), C.byref(o), C.byref(sim), C.byref(a), C.byref(b)))
     as_dict = lambda r: {k: int(getattr(r, k)) for k, _ in SimResultC._fields_}
     return as_dict(a), as_dict(b)
+
+
+# ---------------------------------------------------------------------------
+# transformer layer
+
+def layer_param_shapes(hidden: int):
+    """Shapes of the layer parameters (row-major [in, out] matrices)."""
+    h = int(hidden)
+    return {"norm1": (h,), "wq": (h, h), "wk": (h, h), "wv": (h, h), "wo": (h, h), "norm2": (h,),
+            "w_up": (h, 4 * h), "w_down": (4 * h, h)}
+
+
+class Layer:
+    """One transformer layer over a fixed packed batch (see dcp_layer_fwd /
+    dcp_layer_bwd): ``weights`` bf16 and ``grads`` fp32 device tensors keyed
+    by LAYER_PARAMS.  ``fwd(x, keep)`` returns the output and keeps the
+    activation stash when ``keep``; ``bwd(x, dout)`` returns dx, adding the
+    weight gradients into ``grads`` and recomputing the forward first when
+    no stash was kept."""
+
+    def __init__(self, weights, grads, cu_seqlens, n_heads: int, head_dim: int, causal: bool = False,
+                 scale: Optional[float] = None, eps: float = 1e-6):
+        import torch
+        self.torch = torch
+        self.weights, self.grads = weights, grads
+        cu = _host_cu(cu_seqlens)
+        T = int(cu[-1])
+        self.T, self.hidden = T, n_heads * head_dim
+        self.scale = 1.0 / math.sqrt(head_dim) if scale is None else scale
+        self.d = _Desc(cu, T, n_heads, head_dim, self.scale, causal)
+        self.desc = LayerDescC(C.pointer(self.d.desc), float(eps))
+        lib = self.lib = load()
+        s, f, b = C.c_size_t(), C.c_size_t(), C.c_size_t()
+        _check(lib.dcp_layer_sizes(C.byref(self.desc), C.byref(s), C.byref(f), C.byref(b)))
+        self.stash_bytes, self.fwd_ws_bytes, self.bwd_ws_bytes = s.value, f.value, b.value
+        dev = weights["wq"].device
+        self.w = LayerWeightsC(*[weights[n].data_ptr() for n in LAYER_PARAMS])
+        self.g = LayerWeightsC(*[grads[n].data_ptr() for n in LAYER_PARAMS])
+        self.ws = torch.empty(max(self.fwd_ws_bytes, self.bwd_ws_bytes), dtype=torch.uint8, device=dev)
+        self.stream = _stream_ptr(torch, dev)
+        self.stash = None
+
+    def fwd(self, x, keep: bool = True, out=None):
+        t = self.torch
+        out = t.empty_like(x) if out is None else out
+        self.stash = t.empty(self.stash_bytes, dtype=t.uint8, device=x.device) if keep else None
+        _check(self.lib.dcp_layer_fwd(C.byref(self.desc), C.byref(self.w), x.data_ptr(), out.data_ptr(),
+                                      None if self.stash is None else self.stash.data_ptr(), self.ws.data_ptr(),
+                                      self.ws.numel(), self.stream))
+        return out
+
+    def bwd(self, x, dout, dx=None):
+        t = self.torch
+        dx = t.empty_like(x) if dx is None else dx
+        _check(self.lib.dcp_layer_bwd(C.byref(self.desc), C.byref(self.w), x.data_ptr(), dout.data_ptr(),
+                                      dx.data_ptr(), C.byref(self.g),
+                                      None if self.stash is None else self.stash.data_ptr(), self.ws.data_ptr(),
+                                      self.ws.numel(), self.stream))
+        self.stash = None
+        return dx

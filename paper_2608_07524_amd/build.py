@@ -20,7 +20,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdcp.so")
 
-SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "dcp_api.cpp", "dcp_plan.cpp"]
+SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "layer.hip", "dcp_api.cpp", "dcp_plan.cpp", "layer_api.cpp"]
 
 # Packed fp32 vector ops stay disabled for device code (plain scalar fp32
 # VALU only); the host pass reports the feature as unknown, which is benign.
@@ -54,14 +54,15 @@ def build(verbose: bool = False, extra=(), out: str = LIB, build_dir: str = BUIL
     hipcc = _hipcc()
     os.makedirs(build_dir, exist_ok=True)
     objs = [os.path.join(build_dir, os.path.splitext(s)[0] + ".o") for s in SOURCES]
-    with ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
+    with ThreadPoolExecutor(max_workers=min(6, len(SOURCES))) as ex:
         logs = list(ex.map(lambda so: _compile(hipcc, so[0], so[1], list(extra)), zip(SOURCES, objs)))
     if verbose:
         for s, log in zip(SOURCES, logs):
             if log.strip():
                 print(f"--- {s}\n{log}", file=sys.stderr)
     tmp = out + ".tmp"
-    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
+    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs, "-L/opt/rocm/lib", "-lrocblas",
+           "-Wl,-rpath,/opt/rocm/lib"]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stderr}")

@@ -1,0 +1,97 @@
+"""GPU parity of the transformer layer (dcp_layer_fwd / dcp_layer_bwd, rocBLAS
+GEMMs around the HIP attention and norm kernels) against the float64 layer
+oracle, and the recomputation contract: a backward that re-runs the forward
+returns bitwise what a backward with the stashed activations returns.
+
+Tolerance: every output, input gradient and weight gradient within 2e-2 of
+the largest reference magnitude of its tensor.  The forward stores seven
+intermediates in bf16 (y1; q, k, v; o; h; y2; u; a), each rounded to within
+2^-8 relative, and the GEMMs take bf16 operands; the gradients are bounded
+the same way as the attention gradients."""
+
+import math
+
+import numpy as np
+import pytest
+
+from oracle import layer as LY
+from paper_2608_07524_amd import inputs as I
+
+from gpu_util import GRAD_TOL, to_bits
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    t = pytest.importorskip("torch")
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_07524_amd as P
+    P.load()
+    return t
+
+
+def _dev(torch, a):
+    return torch.from_numpy(I.bf16_bits(np.asarray(a, dtype=np.float32)).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def _setup(torch, lengths, H, D, causal, seed):
+    import paper_2608_07524_amd as P
+    rng = np.random.default_rng(seed)
+    h = H * D
+    cu = I.cu_from_lengths(lengths)
+    T = int(cu[-1])
+    W = {}
+    for n, shape in P.layer_param_shapes(h).items():
+        if n.startswith("norm"):
+            W[n] = 1.0 + 0.2 * rng.standard_normal(shape)
+        else:
+            W[n] = rng.standard_normal(shape) / math.sqrt(shape[0])
+    x = rng.standard_normal((T, h))
+    dout = rng.standard_normal((T, h))
+    # the bf16 values the GPU sees, widened for the oracle
+    Wb = {n: I.bf16_to_f64(I.bf16_bits(v.astype(np.float32))) for n, v in W.items()}
+    xb, db = (I.bf16_to_f64(I.bf16_bits(v.astype(np.float32))) for v in (x, dout))
+    wd = {n: _dev(torch, v) for n, v in Wb.items()}
+    gd = {n: torch.zeros(v.shape, dtype=torch.float32, device="cuda") for n, v in Wb.items()}
+    layer = P.Layer(wd, gd, cu, H, D, causal, 1.0 / math.sqrt(D), 1e-6)
+    return layer, cu, Wb, xb, db, _dev(torch, xb), _dev(torch, db)
+
+
+def _run(torch, layer, x, dout, keep):
+    for g in layer.grads.values():
+        g.zero_()
+    out = layer.fwd(x, keep=keep)
+    dx = layer.bwd(x, dout)
+    torch.cuda.synchronize()
+    return to_bits(out), to_bits(dx), {n: g.cpu().numpy().copy() for n, g in layer.grads.items()}
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_layer_matches_oracle(torch, causal):
+    lengths = [300, 45, 17, 700, 1, 130]
+    H, D = 2, 64
+    layer, cu, Wb, xb, db, x, dout = _setup(torch, lengths, H, D, causal, 21 + causal)
+    out, dx, grads = _run(torch, layer, x, dout, keep=True)
+    ref_out, cache = LY.layer_forward(xb, Wb, cu, H, D, 1.0 / math.sqrt(D), causal, 1e-6)
+    ref_dx, ref_g = LY.layer_backward(db, Wb, cache, cu, H, D, 1.0 / math.sqrt(D), causal)
+
+    def rel(got, ref):
+        return float(np.max(np.abs(got - ref)) / np.max(np.abs(ref)))
+
+    errs = {"out": rel(I.bf16_to_f64(out), ref_out), "dx": rel(I.bf16_to_f64(dx), ref_dx)}
+    errs.update({n: rel(grads[n].astype(np.float64), ref_g[n]) for n in LY.PARAMS})
+    print(f"layer causal={causal}: " + " ".join(f"{k} {v:.1e}" for k, v in errs.items()), flush=True)
+    assert max(errs.values()) <= GRAD_TOL, errs
+
+
+def test_recompute_is_bitwise_the_stashed_backward(torch):
+    layer, cu, Wb, xb, db, x, dout = _setup(torch, [200, 37, 513, 9], 4, 72, False, 5)
+    kept = _run(torch, layer, x, dout, keep=True)
+    again = _run(torch, layer, x, dout, keep=True)
+    recomputed = _run(torch, layer, x, dout, keep=False)
+    for a, b, c in zip(kept[:2], again[:2], recomputed[:2]):
+        assert np.array_equal(a, b) and np.array_equal(a, c)
+    for n in LY.PARAMS:
+        assert np.array_equal(kept[2][n], again[2][n]) and np.array_equal(kept[2][n], recomputed[2][n]), n
