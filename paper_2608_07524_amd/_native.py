@@ -447,7 +447,7 @@ class Layer:
     no stash was kept."""
 
     def __init__(self, weights, grads, cu_seqlens, n_heads: int, head_dim: int, causal: bool = False,
-                 scale: Optional[float] = None, eps: float = 1e-6):
+                 scale: Optional[float] = None, eps: float = 1e-6, workspace=None):
         import torch
         self.torch = torch
         self.weights, self.grads = weights, grads
@@ -464,14 +464,22 @@ class Layer:
         dev = weights["wq"].device
         self.w = LayerWeightsC(*[weights[n].data_ptr() for n in LAYER_PARAMS])
         self.g = LayerWeightsC(*[grads[n].data_ptr() for n in LAYER_PARAMS])
-        self.ws = torch.empty(max(self.fwd_ws_bytes, self.bwd_ws_bytes), dtype=torch.uint8, device=dev)
+        need = max(self.fwd_ws_bytes, self.bwd_ws_bytes)
+        if workspace is not None and workspace.numel() < need:
+            raise ValueError(f"layer workspace needs {need} bytes")
+        # (several layers of one shape may share one workspace: calls on a stream run in order)
+        self.ws = torch.empty(need, dtype=torch.uint8, device=dev) if workspace is None else workspace
         self.stream = _stream_ptr(torch, dev)
         self.stash = None
 
-    def fwd(self, x, keep: bool = True, out=None):
+    def fwd(self, x, keep: bool = True, out=None, stash=None):
+        """``stash``: a preallocated buffer of stash_bytes to keep into."""
         t = self.torch
         out = t.empty_like(x) if out is None else out
-        self.stash = t.empty(self.stash_bytes, dtype=t.uint8, device=x.device) if keep else None
+        if keep:
+            self.stash = t.empty(self.stash_bytes, dtype=t.uint8, device=x.device) if stash is None else stash
+        else:
+            self.stash = None
         _check(self.lib.dcp_layer_fwd(C.byref(self.desc), C.byref(self.w), x.data_ptr(), out.data_ptr(),
                                       None if self.stash is None else self.stash.data_ptr(), self.ws.data_ptr(),
                                       self.ws.numel(), self.stream))

@@ -95,3 +95,23 @@ def test_recompute_is_bitwise_the_stashed_backward(torch):
         assert np.array_equal(a, b) and np.array_equal(a, c)
     for n in LY.PARAMS:
         assert np.array_equal(kept[2][n], again[2][n]) and np.array_equal(kept[2][n], recomputed[2][n]), n
+
+
+def test_stack_executor_recompute_patterns(torch):
+    """Three layers: every recompute pattern (the planner's flags) gives the
+    same input gradient and weight gradients, bit for bit."""
+    from paper_2608_07524_amd import model as M
+    st = M.Stack(3, [0, 150, 170, 400], 2, 64, causal=True, seed=4)
+    results = []
+    for flags in ([0, 0, 0], [1, 0, 0], [1, 1, 0], [1, 1, 1]):
+        for layer in st.layers:
+            for g in layer.grads.values():
+                g.zero_()
+        st.step(flags)
+        torch.cuda.synchronize()
+        dx = to_bits(st.dys[0])  # the first layer's input gradient
+        grads = [layer.grads[n].cpu().numpy().copy() for layer in st.layers for n in LY.PARAMS]
+        results.append((dx, grads, to_bits(st.xs[-1])))
+    for dx, grads, out in results[1:]:
+        assert np.array_equal(dx, results[0][0]) and np.array_equal(out, results[0][2])
+        assert all(np.array_equal(a, b) for a, b in zip(grads, results[0][1]))
