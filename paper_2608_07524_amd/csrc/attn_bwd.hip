@@ -816,7 +816,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
 
 template <int D, bool CAUSAL, bool PACKED>
 hipError_t launch_dkdv_list(const BwdArgs& a, const WorkUnit* units, int n_units) {
-  constexpr DkdvShape sh = bwd_dkdv_shape(D);
+  constexpr DkdvShape sh = PACKED ? bwd_dkdv_window_shape(D) : bwd_dkdv_shape(D);
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, sh.kb, sh.waves, sh.bm, sh.stages, sh.waves_per_eu, CAUSAL, PACKED>),
                      dim3(n_units), dim3(64 * sh.waves), 0, a.stream, static_cast<const __bf16*>(a.q),
                      static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
@@ -829,8 +829,9 @@ hipError_t launch_dkdv_list(const BwdArgs& a, const WorkUnit* units, int n_units
 
 template <int D, bool CAUSAL, bool PACKED>
 hipError_t launch_dq_list(const BwdArgs& a, const WorkUnit* units, int n_units) {
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, kBwdDqWaves, (D > 96 ? 2 : 3), CAUSAL, PACKED>), dim3(n_units),
-                     dim3(64 * kBwdDqWaves), 0, a.stream, static_cast<const __bf16*>(a.q),
+  constexpr int NW = PACKED ? kWinDqWaves : kBwdDqWaves;
+  constexpr int NS = D > 96 ? 2 : (PACKED ? kWinDqStages : 3);
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NW, NS, CAUSAL, PACKED>), dim3(n_units), dim3(64 * NW), 0, a.stream, static_cast<const __bf16*>(a.q),
                      static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
                      static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dq),
                      static_cast<const __bf16*>(a.consts), units, static_cast<const uint64_t*>(a.qwindow_starts),
@@ -888,6 +889,11 @@ int bwd_key_tile_rows(int head_dim) {
   return 32 * sh.kb * sh.waves;
 }
 int bwd_query_tile_rows(int head_dim) { return 32 * kBwdDqWaves; }
+int bwd_key_window_rows(int head_dim) {
+  const DkdvShape sh = bwd_dkdv_window_shape(head_dim);
+  return 32 * sh.kb * sh.waves;
+}
+int bwd_query_window_rows(int head_dim) { return 32 * kWinDqWaves; }
 
 hipError_t launch_bwd(const BwdArgs& a) {
   switch (a.head_dim) {

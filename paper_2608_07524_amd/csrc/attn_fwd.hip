@@ -43,7 +43,7 @@ constexpr int kFwdBN = 64;
 #endif
 // Ring depth: tile kt + kFwdStages - 1 streams in while tile kt is consumed.
 constexpr int kFwdStages = DCP_FWD_STAGES;
-static_assert(kFwdStages >= 3, "tiles kt and kt + 1 are read while kt + 2 lands");
+static_assert(kFwdStages >= 3 && kWinFwdStages >= 3, "tiles kt and kt + 1 are read while kt + 2 lands");
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 constexpr float kNoMax = -1e30f;       // running max before any key
 
@@ -79,7 +79,7 @@ constexpr int kSchedDsRead = 0x100;
 #define DCP_FWD_OCCUPANCY
 #endif
 
-template <int D, int NW, bool CAUSAL, bool PACKED>
+template <int D, int NW, bool CAUSAL, bool PACKED, int STAGES>
 __global__ __launch_bounds__(64 * NW) DCP_FWD_OCCUPANCY void attn_fwd_kernel(const __bf16* __restrict__ q,
                                                            const __bf16* __restrict__ k,
                                                            const __bf16* __restrict__ v, __bf16* __restrict__ o,
@@ -93,7 +93,7 @@ __global__ __launch_bounds__(64 * NW) DCP_FWD_OCCUPANCY void attn_fwd_kernel(con
   constexpr int BN = kFwdBN;
   constexpr int KBUF = BN * KSTR, VBUF = BN * VSTR;
   // as deep as asked, within the 160 KB of LDS
-  constexpr int NST = kFwdStages * 2 * (KBUF + VBUF) <= 163840 ? kFwdStages : 163840 / (2 * (KBUF + VBUF));
+  constexpr int NST = STAGES * 2 * (KBUF + VBUF) <= 163840 ? STAGES : 163840 / (2 * (KBUF + VBUF));
   static_assert(NST >= 3, "ring too shallow");
   using DK = DmaTile<BN, KSTR / 8, CPR, NW>;
   using DV = DmaTile<BN, VSTR / 8, CPR, NW>;
@@ -473,9 +473,9 @@ __global__ __launch_bounds__(64 * NW) DCP_FWD_OCCUPANCY void attn_fwd_kernel(con
   }
 }
 
-template <int D, int NW, bool CAUSAL, bool PACKED>
+template <int D, int NW, bool CAUSAL, bool PACKED, int STAGES>
 hipError_t launch_fwd_list(const FwdArgs& a, const WorkUnit* units, int n_units) {
-  hipLaunchKernelGGL((attn_fwd_kernel<D, NW, CAUSAL, PACKED>), dim3(n_units), dim3(64 * NW), 0, a.stream,
+  hipLaunchKernelGGL((attn_fwd_kernel<D, NW, CAUSAL, PACKED, STAGES>), dim3(n_units), dim3(64 * NW), 0, a.stream,
                      static_cast<const __bf16*>(a.q), static_cast<const __bf16*>(a.k),
                      static_cast<const __bf16*>(a.v), static_cast<__bf16*>(a.o), a.lse,
                      static_cast<const __bf16*>(a.consts), units, static_cast<const uint64_t*>(a.window_starts),
@@ -490,8 +490,9 @@ hipError_t launch_fwd_t(const FwdArgs& a) {
   const WorkUnit* units = static_cast<const WorkUnit*>(a.units);
   if (ev.begin) (void)hipEventRecord(ev.begin, a.stream);
   hipError_t e = hipSuccess;
-  if (a.n_units > 0) e = launch_fwd_list<D, NW, CAUSAL, false>(a, units, a.n_units);
-  if (e == hipSuccess && a.n_wunits > 0) e = launch_fwd_list<D, NW, CAUSAL, true>(a, units + a.n_units, a.n_wunits);
+  if (a.n_units > 0) e = launch_fwd_list<D, NW, CAUSAL, false, kFwdStages>(a, units, a.n_units);
+  if (e == hipSuccess && a.n_wunits > 0)
+    e = launch_fwd_list<D, kWinFwdWaves, CAUSAL, true, kWinFwdStages>(a, units + a.n_units, a.n_wunits);
   if (ev.end) (void)hipEventRecord(ev.end, a.stream);
   return e;
 }
@@ -499,6 +500,7 @@ hipError_t launch_fwd_t(const FwdArgs& a) {
 }  // namespace
 
 int fwd_tile_rows(int head_dim) { return kFwdWaves * 32; }
+int fwd_window_rows(int head_dim) { return kWinFwdWaves * 32; }
 
 hipError_t launch_fwd(const FwdArgs& a) {
   if (a.n_units == 0 && a.n_wunits == 0) return hipSuccess;

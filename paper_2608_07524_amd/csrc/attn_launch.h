@@ -51,6 +51,37 @@ constexpr DkdvShape bwd_dkdv_shape(int head_dim) {
 constexpr int kBwdDqWaves = DCP_BWD_DQ_WAVES;
 constexpr int kBwdDqBN = 64;
 
+// Packed windows (runs of short sequences sharing one tile) launch with
+// their own shape: fewer wavefronts per workgroup (smaller tiles) and a
+// shallower ring, so that two workgroups share a CU; a window then spans at
+// most that many rows.
+#ifndef DCP_WIN_FWD_WAVES
+#define DCP_WIN_FWD_WAVES 4
+#endif
+#ifndef DCP_WIN_FWD_STAGES
+#define DCP_WIN_FWD_STAGES 3
+#endif
+#ifndef DCP_WIN_DQ_WAVES
+#define DCP_WIN_DQ_WAVES 4
+#endif
+#ifndef DCP_WIN_DQ_STAGES
+#define DCP_WIN_DQ_STAGES 2
+#endif
+#ifndef DCP_WIN_DKDV_WAVES
+#define DCP_WIN_DKDV_WAVES 8
+#endif
+#ifndef DCP_WIN_DKDV_STAGES
+#define DCP_WIN_DKDV_STAGES 3
+#endif
+constexpr int kWinFwdWaves = DCP_WIN_FWD_WAVES;
+constexpr int kWinFwdStages = DCP_WIN_FWD_STAGES;
+constexpr int kWinDqWaves = DCP_WIN_DQ_WAVES;
+constexpr int kWinDqStages = DCP_WIN_DQ_STAGES;
+constexpr DkdvShape bwd_dkdv_window_shape(int head_dim) {
+  return head_dim > 96 ? bwd_dkdv_shape(head_dim)
+                       : DkdvShape{1, DCP_WIN_DKDV_WAVES, 64, DCP_WIN_DKDV_STAGES, DCP_DKDV_WPE};
+}
+
 struct FwdArgs {
   const void* q;
   const void* k;
@@ -112,6 +143,10 @@ KernelEvents& kernel_events();
 int fwd_tile_rows(int head_dim);
 int bwd_key_tile_rows(int head_dim);
 int bwd_query_tile_rows(int head_dim);
+// the most rows a packed window of each pass may span
+int fwd_window_rows(int head_dim);
+int bwd_key_window_rows(int head_dim);
+int bwd_query_window_rows(int head_dim);
 hipError_t launch_fwd(const FwdArgs& a);
 hipError_t launch_bwd(const BwdArgs& a);
 

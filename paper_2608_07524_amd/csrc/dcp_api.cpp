@@ -96,10 +96,10 @@ int check_tensor(const void* p, const char* name) {
 
 // Tiles of `tile` rows per (sequence, head), never straddling two
 // sequences, laid out as 8 per-die lists (see unit_for_block).  Runs of
-// consecutive sequences shorter than a tile share one tile as a packed
-// window of at most `tile` rows (each row still attends only within its
-// own sequence), so thousands of short sequences do not each occupy a
-// mostly idle workgroup.  Work of a tile: the keys it visits (forward, dQ
+// consecutive sequences shorter than `window_tile` (<= tile) share one
+// tile as a packed window of at most `window_tile` rows (each row still
+// attends only within its own sequence), so thousands of short sequences do
+// not each occupy a mostly idle workgroup.  Work of a tile: the keys it visits (forward, dQ
 // pass) or the queries visiting it (dK/dV pass); a window's is its row
 // count.  The (sequence, chunk) and window groups -- long sequences split
 // into chunks when a few of them would otherwise leave dies idle -- are
@@ -119,7 +119,7 @@ struct UnitList {
   std::vector<uint64_t> window_starts;  // kWindowWords per packed window
 };
 
-UnitList build_units(const dcp_attn_desc* d, int tile, bool keys_major) {
+UnitList build_units(const dcp_attn_desc* d, int tile, int window_tile, bool keys_major) {
   const int32_t* cu = d->cu_seqlens_host;
   const int32_t H = d->n_heads;
   const int32_t n = d->n_seqs;
@@ -150,13 +150,13 @@ UnitList build_units(const dcp_attn_desc* d, int tile, bool keys_major) {
     }
   };
   for (int32_t b = 0; b < n;) {
-    if (cu[b + 1] - cu[b] >= tile) {
+    if (cu[b + 1] - cu[b] >= window_tile) {
       add_sequence(b++);
       continue;
     }
-    // the run of short sequences from b that fits one tile
+    // the run of short sequences from b that fits one window
     int32_t e = b, nonempty = 0, last = b;
-    while (e < n && cu[e + 1] - cu[e] < tile && cu[e + 1] - cu[b] <= tile) {
+    while (e < n && cu[e + 1] - cu[e] < window_tile && cu[e + 1] - cu[b] <= window_tile) {
       if (cu[e + 1] > cu[e]) {
         ++nonempty;
         last = e;
@@ -352,7 +352,7 @@ extern "C" int dcp_varlen_attn_fwd(const dcp_attn_desc* desc, const void* q, con
     return fail(DCP_ERR_WORKSPACE, "forward workspace needs %zu bytes, got %zu", need, workspace_bytes);
   if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(DCP_ERR_INVALID, "workspace must be 16-byte aligned");
   if ((st = check_device())) return st;
-  const UnitList units = build_units(desc, tile, false);
+  const UnitList units = build_units(desc, tile, fwd_window_rows(desc->head_dim), false);
   if (units.units.empty()) return DCP_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const size_t windows_at = fwd_windows_at(desc);
@@ -382,9 +382,11 @@ extern "C" int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, 
     return fail(DCP_ERR_WORKSPACE, "backward workspace needs %zu bytes, got %zu", l.total, workspace_bytes);
   if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(DCP_ERR_INVALID, "workspace must be 16-byte aligned");
   if ((st = check_device())) return st;
-  const UnitList units = build_units(desc, bwd_key_tile_rows(desc->head_dim), true);
+  const UnitList units =
+      build_units(desc, bwd_key_tile_rows(desc->head_dim), bwd_key_window_rows(desc->head_dim), true);
   if (units.units.empty()) return DCP_OK;
-  const UnitList qunits = build_units(desc, bwd_query_tile_rows(desc->head_dim), false);
+  const UnitList qunits =
+      build_units(desc, bwd_query_tile_rows(desc->head_dim), bwd_query_window_rows(desc->head_dim), false);
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
   if ((st = upload_head({{l.units, l.windows, &units}, {l.qunits, l.qwindows, &qunits}}, workspace, s))) return st;
@@ -405,14 +407,15 @@ extern "C" int dcp_work_list(const dcp_attn_desc* desc, int32_t pass, int32_t* u
   int st = validate_desc(desc);
   if (st) return st;
   if (!n_units || !n_tiles || !n_windows) return fail(DCP_ERR_INVALID, "count outputs are null");
-  int tile = 0;
+  int tile = 0, window = 0;
+  const int D = desc->head_dim;
   switch (pass) {
-    case 0: tile = fwd_tile_rows(desc->head_dim); break;
-    case 1: tile = bwd_key_tile_rows(desc->head_dim); break;
-    case 2: tile = bwd_query_tile_rows(desc->head_dim); break;
+    case 0: tile = fwd_tile_rows(D), window = fwd_window_rows(D); break;
+    case 1: tile = bwd_key_tile_rows(D), window = bwd_key_window_rows(D); break;
+    case 2: tile = bwd_query_tile_rows(D), window = bwd_query_window_rows(D); break;
     default: return fail(DCP_ERR_INVALID, "pass must be 0 (forward), 1 (dK/dV) or 2 (dQ)");
   }
-  const UnitList l = build_units(desc, tile, pass == 1);
+  const UnitList l = build_units(desc, tile, window, pass == 1);
   const size_t nw = l.window_starts.size() / kWindowWords;
   if (units && cap < l.units.size()) return fail(DCP_ERR_INVALID, "units holds %zu, need %zu", cap, l.units.size());
   if (window_starts && cap_windows < nw) return fail(DCP_ERR_INVALID, "window_starts holds %zu, need %zu", cap_windows, nw);

@@ -14,6 +14,11 @@ def _tile_rows(pass_, D):
     return 128 if (pass_ == 1 and D > 96) else 256
 
 
+def _window_rows(pass_, D):
+    """Rows a packed window may span: the window launches' tile."""
+    return 256 if (pass_ == 1 and D <= 96) else 128
+
+
 def _seq_of_rows(cu):
     """Sequence index of every row of the packed batch."""
     lens = np.diff(cu)
@@ -32,7 +37,7 @@ def _decode(starts, x, n):
 def _check(cu, H, D, causal, pass_):
     cu = np.asarray(cu, dtype=np.int64)
     units, n_tiles, starts = N.work_list(cu, H, D, causal, pass_)
-    tile = _tile_rows(pass_, D)
+    tile, wtile = _tile_rows(pass_, D), _window_rows(pass_, D)
     n = units.shape[0]
     assert n_tiles % 8 == 0 and (n - n_tiles) % 8 == 0
     seq_of = _seq_of_rows(cu)
@@ -49,20 +54,20 @@ def _check(cu, H, D, causal, pass_):
             assert seq0 == cu[b] and seqlen == cu[b + 1] - cu[b]
             assert (row0 - seq0) % tile == 0 and rows == min(tile, seqlen - (row0 - seq0))
             continue
-        assert seqlen < 0 and row0 == seq0
+        assert seqlen < 0 and row0 == seq0 and rows <= wtile
         w = -seqlen - 1
         windows_seen[w, head] += 1
-        # whole sequences, each shorter than a tile, at least two of them
+        # whole sequences, each shorter than a window, at least two of them
         bs = np.unique(seq_of[row0:row0 + rows])
         assert cu[bs[0]] == row0 and cu[bs[-1] + 1] == row0 + rows
-        assert np.all(np.diff(cu)[bs] < tile) and bs.size >= 2
+        assert np.all(np.diff(cu)[bs] < wtile) and bs.size >= 2
         for x in range(rows):
             b = int(seq_of[row0 + x])
             assert _decode(starts[w], x, rows) == (cu[b] - row0, cu[b + 1] - row0)
     assert np.all(covered == 1), "a row is covered twice or not at all"
     assert np.all(windows_seen == 1)
-    # no sequence of a tile or more is ever packed
-    long_rows = np.flatnonzero(np.diff(cu)[seq_of] >= tile)
+    # no sequence of a window or more is ever packed
+    long_rows = np.flatnonzero(np.diff(cu)[seq_of] >= wtile)
     for i in range(n_tiles, n):
         row0, rows = units[i, 0], units[i, 3]
         assert not np.any((long_rows >= row0) & (long_rows < row0 + rows))
@@ -94,7 +99,7 @@ def test_transformer_2d_packs(axis):
 
 
 def test_tiny_config_and_edges():
-    _check(I.tiny().cu_seqlens, 4, 64, False, 0)  # 37 + 64 + 128 share one window; 200 runs alone
+    _check(I.tiny().cu_seqlens, 4, 64, False, 0)  # 37 + 64 share one window; 128 and 200 run alone
     _check([0, 0, 0], 2, 72, False, 0)  # only empty sequences
     _check([0, 5], 2, 72, True, 1)  # one short sequence: a plain tile
     _check([0, 128, 256], 1, 128, False, 1)  # two sequences of exactly one dK/dV tile (D 128)
