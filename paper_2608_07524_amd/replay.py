@@ -4,7 +4,10 @@ Appendix B) on synthetic length mixtures (Sec. 4.1, Appendix A shapes).
 
     python -m paper_2608_07524_amd.replay [--devices 32] [--md out.md]
 
-Cost table per model, one row per length the stream uses:
+Cost table per model, one row per length the stream uses (Transformer-1D
+also a second time from the dual-layer profile of the library's whole layer,
+``model.profile_rows``: attention, projections, norms and activation timed
+together on the second of two layers, m = that layer's stash bytes):
 * attention, measured on this GPU through the library: Transformer-1D rows
   come from dcp_profile_cost (one causal sequence of each length, all 48
   heads of width 64); Transformer-2D rows time the forward and backward of a
@@ -161,9 +164,19 @@ def main(argv=None):
     # table's lengths are powers of two, each sequence taking the next one up.
     grid = [128 << i for i in range(11)]
     rows_1d, lin_1d = cost_rows(torch, P, "Transformer-1D", grid)
+    # and from the dual-layer profile of the library's whole layer (the
+    # second of two layers timed, its stash bytes as m), Sec. 3.5
+    from .model import profile_rows
+    L1, h1, H1, D1, _, causal1 = MODELS["Transformer-1D"]
+    rows_1d_layer = [(r.seq_len, r.t_f_ns, r.t_b_ns, r.m_bytes, r.m_inp_bytes)
+                     for r in profile_rows(grid, H1, D1, causal1)]
+    texts = []
     for label, med in (("short", 1024), ("balanced", 4096), ("long", 16384)):
-        lens = I.text_lengths(rng, args.n_seqs, median=med).tolist()
+        texts.append((med, I.text_lengths(rng, args.n_seqs, median=med).tolist()))
+    for med, lens in texts:
         scenarios.append(("Transformer-1D", f"text, median {med}", rows_1d, lens, lin_1d))
+    for med, lens in texts:
+        scenarios.append(("Transformer-1D", f"text, median {med}, layer profile", rows_1d_layer, lens, None))
     # Transformer-2D on video: the long-tail clip mix (frames {1,16,32,51}
     # weighted .4/.3/.2/.1 x 256^2, 480x854, 720x1280), one clip per batch.
     clips = I.video_clips(rng, 64 * 1024 * args.n_seqs, cap=131072)[:args.n_seqs]  # ~30k tokens per clip
