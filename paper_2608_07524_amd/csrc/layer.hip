@@ -51,8 +51,11 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(const __bf16* __restri
 //   dx = res + r * (g*dy - xh * mean(g*dy*xh)),  xh = x * r,
 // and this block's partial sums of dg = sum_rows dy * xh (one row of
 // `partial` per block; a second kernel adds the blocks in a fixed order, so
-// the result is deterministic).  Each wavefront walks kRowsPerWave rows.
-constexpr int kNormBwdRows = 64;  // rows per block (16 per wavefront)
+// the result is deterministic).  Each wavefront walks kNormBwdRows / 4 rows;
+// a lane owns the columns 8*lane + 512*k (k < kNormMaxChunks, h <= 4096) and
+// keeps their dg partials in registers until the block's end.
+constexpr int kNormBwdRows = 16;  // rows per block (4 per wavefront): enough blocks to keep every CU busy
+constexpr int kNormMaxChunks = 8;  // 16-byte column chunks per lane: h <= 64 * 8 * 8
 
 __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const float* __restrict__ dy, const __bf16* __restrict__ x,
                                                           const __bf16* __restrict__ g, const float* __restrict__ rstd,
@@ -60,57 +63,88 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const float* __restric
                                                           float* __restrict__ partial, int64_t rows, int h) {
   extern __shared__ float dg_lds[];  // [4 wavefronts][h]
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int c = threadIdx.x; c < 4 * h; c += 256) dg_lds[c] = 0.f;
-  __syncthreads();
-  float* dgw = dg_lds + wave * h;
+  float acc[kNormMaxChunks][8];
+#pragma unroll
+  for (int k = 0; k < kNormMaxChunks; ++k)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[k][e] = 0.f;
   const int64_t r0 = int64_t(blockIdx.x) * kNormBwdRows + wave * (kNormBwdRows / 4);
   for (int i = 0; i < kNormBwdRows / 4; ++i) {
     const int64_t row = r0 + i;
     if (row >= rows) break;
     const float r = rstd[row];
     float dot = 0.f;
-    for (int c = 8 * lane; c < h; c += 512) {
-      const bf16x8 xv = *reinterpret_cast<const bf16x8*>(x + row * h + c);
-      const bf16x8 gv = *reinterpret_cast<const bf16x8*>(g + c);
-      const f32x4 d0 = *reinterpret_cast<const f32x4*>(dy + row * h + c);
-      const f32x4 d1 = *reinterpret_cast<const f32x4*>(dy + row * h + c + 4);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float d = e < 4 ? d0[e] : d1[e - 4];
-        const float xh = float(xv[e]) * r;
-        dot += float(gv[e]) * d * xh;
-        dgw[c + e] += d * xh;  // lane-private columns: no conflicts between lanes
+    for (int k = 0; k < kNormMaxChunks; ++k) {
+      const int c = 8 * lane + 512 * k;
+      if (c < h) {
+        const bf16x8 xv = *reinterpret_cast<const bf16x8*>(x + row * h + c);
+        const bf16x8 gv = *reinterpret_cast<const bf16x8*>(g + c);
+        const f32x4 d0 = *reinterpret_cast<const f32x4*>(dy + row * h + c);
+        const f32x4 d1 = *reinterpret_cast<const f32x4*>(dy + row * h + c + 4);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float d = e < 4 ? d0[e] : d1[e - 4];
+          const float xh = float(xv[e]) * r;
+          dot += float(gv[e]) * d * xh;
+          acc[k][e] += d * xh;
+        }
       }
     }
     const float mean = wave_sum(dot) / float(h);
-    for (int c = 8 * lane; c < h; c += 512) {
-      const bf16x8 xv = *reinterpret_cast<const bf16x8*>(x + row * h + c);
-      const bf16x8 gv = *reinterpret_cast<const bf16x8*>(g + c);
-      const bf16x8 rv = *reinterpret_cast<const bf16x8*>(res + row * h + c);
-      const f32x4 d0 = *reinterpret_cast<const f32x4*>(dy + row * h + c);
-      const f32x4 d1 = *reinterpret_cast<const f32x4*>(dy + row * h + c + 4);
-      bf16x8 o;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float d = e < 4 ? d0[e] : d1[e - 4];
-        o[e] = __bf16(float(rv[e]) + r * (float(gv[e]) * d - float(xv[e]) * r * mean));
+    for (int k = 0; k < kNormMaxChunks; ++k) {
+      const int c = 8 * lane + 512 * k;
+      if (c < h) {
+        const bf16x8 xv = *reinterpret_cast<const bf16x8*>(x + row * h + c);
+        const bf16x8 gv = *reinterpret_cast<const bf16x8*>(g + c);
+        const bf16x8 rv = *reinterpret_cast<const bf16x8*>(res + row * h + c);
+        const f32x4 d0 = *reinterpret_cast<const f32x4*>(dy + row * h + c);
+        const f32x4 d1 = *reinterpret_cast<const f32x4*>(dy + row * h + c + 4);
+        bf16x8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float d = e < 4 ? d0[e] : d1[e - 4];
+          o[e] = __bf16(float(rv[e]) + r * (float(gv[e]) * d - float(xv[e]) * r * mean));
+        }
+        *reinterpret_cast<bf16x8*>(dx + row * h + c) = o;
       }
-      *reinterpret_cast<bf16x8*>(dx + row * h + c) = o;
     }
+  }
+  float* dgw = dg_lds + wave * h;
+#pragma unroll
+  for (int k = 0; k < kNormMaxChunks; ++k) {
+    const int c = 8 * lane + 512 * k;
+    if (c < h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dgw[c + e] = acc[k][e];
   }
   __syncthreads();
   for (int c = threadIdx.x; c < h; c += 256)
     partial[int64_t(blockIdx.x) * h + c] = dg_lds[c] + dg_lds[h + c] + dg_lds[2 * h + c] + dg_lds[3 * h + c];
 }
 
-// dg[c] += sum over blocks of partial[b][c], blocks in order.
+// dg[c] += sum over blocks of partial[b][c].  A workgroup takes 64 columns;
+// its four wavefronts each sum every fourth partial row, then the four sums
+// are added; the order is fixed, so the result is deterministic.
 __global__ __launch_bounds__(256) void colsum_add_kernel(const float* __restrict__ partial, float* __restrict__ dg,
                                                          int nblocks, int h) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= h) return;
-  float s = 0.f;
-  for (int b = 0; b < nblocks; ++b) s += partial[int64_t(b) * h + c];
-  dg[c] += s;
+  __shared__ float sums[4][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c = blockIdx.x * 64 + lane;
+  // four independent running sums per lane (rows b = 16i + 4j + wave for j
+  // = 0..3), so that loads overlap; added in a fixed order
+  float s4[4] = {0.f, 0.f, 0.f, 0.f};
+  if (c < h) {
+    int b = wave;
+    for (; b + 12 < nblocks; b += 16)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) s4[j] += partial[int64_t(b + 4 * j) * h + c];
+    for (int j = 0; b < nblocks; b += 4, ++j) s4[j & 3] += partial[int64_t(b) * h + c];
+  }
+  sums[wave][lane] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+  __syncthreads();
+  if (wave == 0 && c < h) dg[c] += ((sums[0][lane] + sums[1][lane]) + sums[2][lane]) + sums[3][lane];
 }
 
 // GELU, tanh form: a = u/2 * (1 + tanh(k0 * (u + k1 u^3))).
@@ -170,7 +204,7 @@ hipError_t launch_rmsnorm_bwd(const float* dy, const void* x, const void* g, con
                      static_cast<const __bf16*>(res), static_cast<__bf16*>(dx), partial, rows, h);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(colsum_add_kernel, dim3(unsigned((h + 255) / 256)), dim3(256), 0, s, partial, dg, int(nb), h);
+  hipLaunchKernelGGL(colsum_add_kernel, dim3(unsigned((h + 63) / 64)), dim3(256), 0, s, partial, dg, int(nb), h);
   return hipGetLastError();
 }
 

@@ -41,7 +41,6 @@ class Stack:
                  seed: int = 0, eps: float = 1e-6):
         import torch
         self.torch = torch
-        P = N
         h = n_heads * head_dim
         cu = np.asarray(cu_seqlens, dtype=np.int32)
         T = int(cu[-1])
@@ -50,7 +49,7 @@ class Stack:
         ws = None
         for _ in range(n_layers):
             W, G = {}, {}
-            for name, shape in P.layer_param_shapes(h).items():
+            for name, shape in N.layer_param_shapes(h).items():
                 if name.startswith("norm"):
                     W[name] = torch.ones(shape, dtype=torch.bfloat16, device="cuda")
                 else:
@@ -142,6 +141,7 @@ MODELS = {
 def main(argv=None):
     ap = argparse.ArgumentParser(description="recompute executor and dual-layer profile on this GPU")
     ap.add_argument("--md", default=None)
+    ap.add_argument("--model", default=None, help="only the model whose name starts with this")
     args = ap.parse_args(argv)
     import torch
     if not torch.cuda.is_available():
@@ -149,6 +149,8 @@ def main(argv=None):
     N.load()
     md = []
     for name, (H, D, causal, L, s) in MODELS.items():
+        if args.model and not name.startswith(args.model):
+            continue
         row = profile_rows([s], H, D, causal)[0]
         st = Stack(L, [0, s], H, D, causal)
         curve = []

@@ -39,7 +39,6 @@ from typing import List
 
 import numpy as np
 
-from . import _native as N
 from . import inputs as I
 
 MODELS = {
