@@ -70,8 +70,12 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict
   const int c = threadIdx.x & 15;
   const int64_t n_pairs = int64_t(rows_end) * H;
   float part = 0.f;
+  // pairs are head-major (pair = head * rows_end + row), so the fp32 [H, T]
+  // reads and writes of neighbouring lane groups are neighbouring rows
+  const int64_t row = pair % rows_end;
+  const int hh = int(pair / rows_end);
   if (pair < n_pairs && c < CPR) {
-    const int64_t off = pair * D + 8 * c;
+    const int64_t off = (row * H + hh) * D + 8 * c;
     const bf16x8 a = *reinterpret_cast<const bf16x8*>(dout + off);
     const bf16x8 b = *reinterpret_cast<const bf16x8*>(o + off);
 #pragma unroll
@@ -82,8 +86,6 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict
   part += __shfl_xor(part, 2, 16);
   part += __shfl_xor(part, 1, 16);
   if (pair < n_pairs && c == 0) {
-    const int64_t row = pair / H;
-    const int hh = int(pair % H);
     ndelta[int64_t(hh) * T + row] = -part;
     lse2[int64_t(hh) * T + row] = lse[int64_t(hh) * T + row] * kLog2e;
   }
