@@ -97,3 +97,36 @@ def test_profile_validation():
     rows = (N.CostRow * 2)()
     assert lib.dcp_profile_cost(lens.ctypes.data_as(C.POINTER(C.c_int64)), 2, C.byref(o), 1 << 20, n.value, None,
                                 rows) == N.DCP_ERR_INVALID
+
+
+def test_layer_validation():
+    """Layer calls reject bad descriptors, pointers and workspaces on the host."""
+    lib = P.load()
+    fake = 1 << 20
+
+    def layer_desc(cu, T, H, D, eps=1e-6):
+        d, keep = _desc(cu, T, H=H, D=D)
+        L = N.LayerDescC(C.pointer(d), eps)
+        return L, (d, keep)
+
+    s, f, b = C.c_size_t(), C.c_size_t(), C.c_size_t()
+    L, keep = layer_desc([0, 30, 64], 64, 2, 64)
+    assert lib.dcp_layer_sizes(C.byref(L), C.byref(s), C.byref(f), C.byref(b)) == 0
+    assert s.value >= 30 * 128 * 64 and f.value > s.value and b.value > s.value
+    # hidden = 64 * 128 = 8192 > 4096
+    L2, keep2 = layer_desc([0, 64], 64, 64, 128)
+    assert lib.dcp_layer_sizes(C.byref(L2), C.byref(s), C.byref(f), C.byref(b)) == N.DCP_ERR_UNSUPPORTED
+    # rows outside every sequence
+    L3, keep3 = layer_desc([0, 60], 64, 2, 64)
+    assert lib.dcp_layer_sizes(C.byref(L3), C.byref(s), C.byref(f), C.byref(b)) == N.DCP_ERR_INVALID
+    L4, keep4 = layer_desc([0, 64], 64, 2, 64, eps=-1.0)
+    assert lib.dcp_layer_sizes(C.byref(L4), C.byref(s), C.byref(f), C.byref(b)) == N.DCP_ERR_INVALID
+    # null weights, misaligned input, short workspace: rejected before any device work
+    lib.dcp_layer_sizes(C.byref(L), C.byref(s), C.byref(f), C.byref(b))
+    w = N.LayerWeightsC(*([fake] * 8))
+    w_null = N.LayerWeightsC(*([fake] * 7 + [None]))
+    assert lib.dcp_layer_fwd(C.byref(L), C.byref(w_null), fake, fake, None, fake, f.value, None) == N.DCP_ERR_INVALID
+    assert lib.dcp_layer_fwd(C.byref(L), C.byref(w), fake + 8, fake, None, fake, f.value, None) == N.DCP_ERR_INVALID
+    assert lib.dcp_layer_fwd(C.byref(L), C.byref(w), fake, fake, None, fake, f.value - 1, None) == N.DCP_ERR_WORKSPACE
+    assert lib.dcp_layer_bwd(C.byref(L), C.byref(w), fake, fake, fake, C.byref(w), None, fake, b.value - 1, None) \
+        == N.DCP_ERR_WORKSPACE
