@@ -53,8 +53,8 @@ constexpr int kBwdDqBN = 64;
 
 // Packed windows (runs of short sequences sharing one tile) launch with
 // their own shape: fewer wavefronts per workgroup (smaller tiles) and a
-// shallower ring, so that two workgroups share a CU; a window then spans at
-// most that many rows.
+// shallower ring -- for the dK/dV pass also 32-query ring tiles -- so that
+// two workgroups share a CU; a window then spans at most that many rows.
 #ifndef DCP_WIN_FWD_WAVES
 #define DCP_WIN_FWD_WAVES 4
 #endif
@@ -68,10 +68,13 @@ constexpr int kBwdDqBN = 64;
 #define DCP_WIN_DQ_STAGES 2
 #endif
 #ifndef DCP_WIN_DKDV_WAVES
-#define DCP_WIN_DKDV_WAVES 8
+#define DCP_WIN_DKDV_WAVES 4
 #endif
 #ifndef DCP_WIN_DKDV_STAGES
 #define DCP_WIN_DKDV_STAGES 3
+#endif
+#ifndef DCP_WIN_DKDV_BM
+#define DCP_WIN_DKDV_BM 32
 #endif
 constexpr int kWinFwdWaves = DCP_WIN_FWD_WAVES;
 constexpr int kWinFwdStages = DCP_WIN_FWD_STAGES;
@@ -79,7 +82,7 @@ constexpr int kWinDqWaves = DCP_WIN_DQ_WAVES;
 constexpr int kWinDqStages = DCP_WIN_DQ_STAGES;
 constexpr DkdvShape bwd_dkdv_window_shape(int head_dim) {
   return head_dim > 96 ? bwd_dkdv_shape(head_dim)
-                       : DkdvShape{1, DCP_WIN_DKDV_WAVES, 64, DCP_WIN_DKDV_STAGES, DCP_DKDV_WPE};
+                       : DkdvShape{1, DCP_WIN_DKDV_WAVES, DCP_WIN_DKDV_BM, DCP_WIN_DKDV_STAGES, DCP_DKDV_WPE};
 }
 
 struct FwdArgs {

@@ -16,7 +16,7 @@ def _tile_rows(pass_, D):
 
 def _window_rows(pass_, D):
     """Rows a packed window may span: the window launches' tile."""
-    return 256 if (pass_ == 1 and D <= 96) else 128
+    return 128
 
 
 def _seq_of_rows(cu):
