@@ -185,29 +185,49 @@ __device__ __forceinline__ void to_mfma16_layout(bf16x8& xv, bf16x8& yv) {
 // dP - Delta directly.  With KB = 2 every operand fetched from LDS feeds
 // two matrix products, and the exponentials of one key block can overlap
 // the products of the other.
-template <int D, int KB, int NW, int BM, int NSTAGE, int WPE, bool CAUSAL, bool PACKED>
+//
+// FUSED (packed windows, 32-query tiles, one 32-key block per wavefront):
+// the workgroup holds every key of the queries it visits, so it also
+// computes dQ = scale * dS K.  Each wavefront writes its bf16 dS^T block
+// (32 keys x the tile's 32 queries) into an LDS matrix of the window's keys
+// x 32 queries (two buffers, alternating per tile); after the tile's
+// barrier the wavefronts split the tile's 16x16 dQ output blocks, reading dS
+// and a copy of the window's K (both by transposing reads) from LDS.  To
+// fit two workgroups per CU the ring then holds Q and dO once, at the
+// row-read stride, and the transposing reads of dV and dK use that copy.
+template <int D, int KB, int NW, int BM, int NSTAGE, int WPE, bool CAUSAL, bool PACKED, bool FUSED>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) void attn_bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
-    __bf16* __restrict__ dk, __bf16* __restrict__ dv, const __bf16* __restrict__ consts,
+    __bf16* __restrict__ dk, __bf16* __restrict__ dv, __bf16* __restrict__ dq, const __bf16* __restrict__ consts,
     const WorkUnit* __restrict__ units, const uint64_t* __restrict__ window_starts, int per_xcd, int H, int T,
     float scale, float scale_log2) {
   using S = BwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
   constexpr int RSTR = S::DP + 8;  // an odd number of 16-byte chunks
-  constexpr int TSTR = S::TSTR;
+  constexpr int TSTR = FUSED ? RSTR : S::TSTR;  // (fused: the one copy serves both reads)
   static_assert(BM % 32 == 0, "whole 32-query blocks per tile");
+  static_assert(!FUSED || (PACKED && KB == 1 && BM == 32), "fused dQ: packed windows, 32-query tiles, KB 1");
   using DR = DmaTile<BM, RSTR / 8, CPR, NW>;
   using DT = DmaTile<BM, TSTR / 8, CPR, NW>;
   using DL = DmaVecPair<BM, NW>;
-  constexpr int NI = 2 * DR::NI + 2 * DT::NI + DL::NI;  // copies per wavefront per tile
-  constexpr int RBUF = DR::ELEMS, TBUF = DT::ELEMS;
+  constexpr int NI = FUSED ? 2 * DR::NI + DL::NI : 2 * DR::NI + 2 * DT::NI + DL::NI;  // copies per wavefront per tile
+  constexpr int RBUF = DR::ELEMS, TBUF = FUSED ? 0 : DT::ELEMS;
   constexpr int SSTR = S::RSTR;  // epilogue staging stride
+  // fused dQ: the window's K rows for transposing reads, and dS^T
+  constexpr int NKEY = 32 * NW;
+  constexpr int KTSTR = S::TSTR;  // 64 mod 128 bytes
+  using DKT = DmaTile<NKEY, KTSTR / 8, CPR, NW>;
+  constexpr int KTBUF = FUSED ? DKT::ELEMS : 0;
+  constexpr int DSBUF = FUSED ? NKEY * BM : 0;  // one buffer: [key][query], rows of 64 bytes
+  constexpr int NMQ = (D + 15) / 16;            // 16-column blocks of dQ
   __shared__ __attribute__((aligned(16))) __bf16 Qr[NSTAGE * RBUF];
   __shared__ __attribute__((aligned(16))) __bf16 dOr[NSTAGE * RBUF];
-  __shared__ __attribute__((aligned(16))) __bf16 Qt[NSTAGE * TBUF];
-  __shared__ __attribute__((aligned(16))) __bf16 dOt[NSTAGE * TBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 Qt[FUSED ? 8 : NSTAGE * TBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 dOt[FUSED ? 8 : NSTAGE * TBUF];
   __shared__ __attribute__((aligned(16))) float LV[NSTAGE * 2 * BM];  // LSE*log2e | -Delta
+  __shared__ __attribute__((aligned(16))) __bf16 Kt[FUSED ? KTBUF : 8];
+  __shared__ __attribute__((aligned(16))) __bf16 dSt[FUSED ? 2 * DSBUF : 8];
   constexpr int NSB = NW * KB;  // 32-key blocks per workgroup
   static_assert(NSB % 2 == 0 && NSTAGE * RBUF >= NSB / 2 * 32 * SSTR, "staging area too small");
   static_assert(NSTAGE == 2 || NSTAGE == 3, "ring depth");
@@ -256,6 +276,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
     }
   }
   wait_vmcnt<0>();  // settle the fragment loads before the first copy
+  // (fused) the window's keys, rows past its end zero; issued before the
+  // first ring tile, so the first ring wait covers it
+  if constexpr (FUSED) DKT::issue(Kt, kh + int64_t(key_t0) * ts, ts, u.rows, zero, zero, wave, lane);
 
   const int wave_key_lo = key_t0 + 32 * KB * wave;  // smallest key of this wavefront
   // queries of each key's sequence: [q_lo, q_hi)
@@ -285,14 +308,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
     const __bf16* ds = doh + int64_t(q0) * ts;
     if (kFullCopies && valid >= BM) {
       DR::issue_full(&Qr[st * RBUF], qs, fo_r, wave);
-      DT::issue_full(&Qt[st * TBUF], qs, fo_t, wave);
+      if constexpr (!FUSED) DT::issue_full(&Qt[st * TBUF], qs, fo_t, wave);
       DR::issue_full(&dOr[st * RBUF], ds, fo_r, wave);
-      DT::issue_full(&dOt[st * TBUF], ds, fo_t, wave);
+      if constexpr (!FUSED) DT::issue_full(&dOt[st * TBUF], ds, fo_t, wave);
     } else {
       DR::issue(&Qr[st * RBUF], qs, ts, valid, zero, zero, wave, lane);
-      DT::issue(&Qt[st * TBUF], qs, ts, valid, zero, zero, wave, lane);
+      if constexpr (!FUSED) DT::issue(&Qt[st * TBUF], qs, ts, valid, zero, zero, wave, lane);
       DR::issue(&dOr[st * RBUF], ds, ts, valid, zero, zero, wave, lane);
-      DT::issue(&dOt[st * TBUF], ds, ts, valid, zero, zero, wave, lane);
+      if constexpr (!FUSED) DT::issue(&dOt[st * TBUF], ds, ts, valid, zero, zero, wave, lane);
     }
     // A query past the sequence end gets LSE = +inf, so its P is exactly 0.
     DL::issue(&LV[st * 2 * BM], lseh + q0, ndh + q0, valid, finf, fzero, wave, lane);
@@ -340,9 +363,61 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
               : (4 * g + ((lane & 15) >> 2)) * TSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const lds_bf16* Qr3 = lds_ptr(Qr);
   const lds_bf16* dOr3 = lds_ptr(dOr);
-  const lds_bf16* Qt3 = lds_ptr(Qt);
-  const lds_bf16* dOt3 = lds_ptr(dOt);
+  const lds_bf16* Qt3 = FUSED ? Qr3 : lds_ptr(Qt);
+  const lds_bf16* dOt3 = FUSED ? dOr3 : lds_ptr(dOt);
   const lds_f32* LV3 = lds_ptr(LV);
+  constexpr unsigned TBUF_R = FUSED ? RBUF : TBUF;  // stage size of the transposing-read copies
+
+  // (fused) this lane's four 8-byte slots of the dS^T buffer of tile it:
+  // key 32*wave + j, queries 8b + 4g .. +3 for b = 0..3 at bf16x4 index 2b
+  typedef DCP_LDS bf16x4 lds_bf16x4;
+  auto ds_slots = [&](int it) DCP_INLINE {
+    return (lds_bf16x4*)(lds_ptr(dSt) + (unsigned(it) & 1u) * DSBUF + (32 * wave + j) * BM + 4 * g);
+  };
+  // (fused) a wavefront with no work in tile it still owns its rows of dS^T
+  auto zero_ds = [&](int it) DCP_INLINE {
+    if constexpr (FUSED) {
+      lds_bf16x4* row = ds_slots(it);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) row[2 * b] = bf16x4{};
+    }
+  };
+  // (fused) dQ of tile it once every wavefront's dS^T is in LDS, as dQ^T =
+  // K^T dS^T in 16x16 blocks: block x = (16-column block nd, 16-query half
+  // mq) goes to wavefront x % NW.  A = K^T (columns x keys) and B = dS^T
+  // (keys x queries) both come from transposing reads of key-major rows,
+  // with the contraction index of lane group g4 = keys 32*ks + 8*g4 .. +7
+  // on both sides; lane (g4, i) ends with query 16*mq + i, columns
+  // 16*nd + 4*g4 .. +3 (one 8-byte store).
+  __bf16* dqh = dq + int64_t(u.seq0) * ts + int64_t(h) * D;
+  auto dq_phase = [&](int it) DCP_INLINE {
+    if constexpr (FUSED) {
+      const int q0 = q_begin + it * BM;
+      const int l16 = lane & 15, g4q = lane >> 4;
+      const lds_bf16* ds3 = lds_ptr(dSt) + (unsigned(it) & 1u) * DSBUF + (8 * g4q + (l16 >> 2)) * BM + 4 * (l16 & 3);
+      const lds_bf16* kt3 = lds_ptr(Kt) + (8 * g4q + (l16 >> 2)) * KTSTR + 4 * (l16 & 3);
+      for (int x = wave; x < 2 * NMQ; x += NW) {
+        const int nd = x >> 1, mq = x & 1;
+        f32x4 acc = {};
+#pragma unroll
+        for (int ks = 0; ks < NW; ++ks) {
+          const lds_bf16* pk = kt3 + 32 * ks * KTSTR + 16 * nd;
+          const lds_bf16* pd = ds3 + 32 * ks * BM + 16 * mq;
+          acc = mfma16(cat(lds_read_tr(pk), lds_read_tr(pk + 4 * KTSTR)), cat(lds_read_tr(pd), lds_read_tr(pd + 4 * BM)),
+                       acc);
+        }
+        const int qq = q0 + 16 * mq + l16;
+        const int d0 = 16 * nd + 4 * g4q;
+        if (qq < seqlen && d0 < D) {
+          bf16x4 w;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) w[r] = __bf16(acc[r] * scale);
+          *reinterpret_cast<bf16x4*>(dqh + int64_t(qq) * ts + d0) = w;
+        }
+      }
+    }
+  };
+  int ds_it = 0;  // (fused) the tile whose dS^T process_block writes
 
   // One 32-query block (first query qa, sequence-relative) of stage st
   // against this wavefront's 32*KB keys.  MASK 1 applies the causal mask,
@@ -350,7 +425,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   auto process_block = [&](unsigned st, int qb, int qa, auto mask_tag) DCP_INLINE {
     constexpr int MASK = decltype(mask_tag)::value;
     unsigned rb = st * RBUF + 32 * qb * RSTR + ar_off;
-    unsigned tb = st * TBUF + 32 * qb * TSTR + tr_off;
+    unsigned tb = st * TBUF_R + 32 * qb * TSTR + tr_off;
     unsigned lb = st * 2 * BM + 32 * qb + 4 * g;
     // Opaque to the optimizer: each read below is then one of these bases
     // plus a constant, which folds into the instruction's offset field
@@ -403,6 +478,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
           pa[kb][b >> 1][4 * (b & 1) + c] = __bf16(p);
           da[kb][b >> 1][4 * (b & 1) + c] = __bf16(p * dp[kb][r]);
         }
+    }
+    if constexpr (FUSED) {
+      lds_bf16x4* row = ds_slots(ds_it);
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        row[2 * b] = bf16x4{da[0][b >> 1][4 * (b & 1)], da[0][b >> 1][4 * (b & 1) + 1], da[0][b >> 1][4 * (b & 1) + 2],
+                            da[0][b >> 1][4 * (b & 1) + 3]};
     }
     if constexpr (S::KV16) {
       // dV += P^T dO and dK += dS^T Q in 16x16 blocks: each B fragment (16
@@ -468,10 +550,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
       if (it + NSTAGE - 1 < n_qt) issue_tile(it + NSTAGE - 1);
       const unsigned st = unsigned(it) % NSTAGE;
       const int q0 = q_begin + it * BM;
+      ds_it = it;
 #pragma unroll
       for (int qb = 0; qb < BM / 32; ++qb) {
         const int qa = q0 + 32 * qb;
-        if (qa >= seqlen) continue;  // padding rows of the last tile
+        if (qa >= seqlen) {  // padding rows of the last tile
+          zero_ds(it);
+          continue;
+        }
         if (MASK == 1) {
           if (qa + 31 < wave_key_lo) continue;  // every query precedes every key
           if (qa >= wave_key_lo + 32 * KB - 1) {
@@ -479,19 +565,26 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
             continue;
           }
         }
-        if (MASK == 2 && (qa + 31 < wq_lo || qa >= wq_hi)) continue;  // no query of these keys' sequences
+        if (MASK == 2 && (qa + 31 < wq_lo || qa >= wq_hi)) {  // no query of these keys' sequences
+          zero_ds(it);
+          continue;
+        }
         process_block(st, qb, qa, std::integral_constant<int, MASK>{});
       }
       wait_next(it);
       __syncthreads();
+      dq_phase(it);
     }
   };
-  // no key of this wavefront in the tile: copies and barriers only
+  // no key of this wavefront in the tile: copies and barriers only (and,
+  // fused, zero dS^T rows and a share of the tile's dQ)
   auto idle = [&](int it0, int it1) DCP_INLINE {
     for (int it = it0; it < it1; ++it) {
       if (it + NSTAGE - 1 < n_qt) issue_tile(it + NSTAGE - 1);
+      zero_ds(it);
       wait_next(it);
       __syncthreads();
+      dq_phase(it);
     }
   };
   if (32 * KB * wave < u.rows) {
@@ -816,14 +909,15 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   }
 }
 
-template <int D, bool CAUSAL, bool PACKED>
+template <int D, bool CAUSAL, bool PACKED, bool FUSED = false>
 hipError_t launch_dkdv_list(const BwdArgs& a, const WorkUnit* units, int n_units) {
   constexpr DkdvShape sh = PACKED ? bwd_dkdv_window_shape(D) : bwd_dkdv_shape(D);
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, sh.kb, sh.waves, sh.bm, sh.stages, sh.waves_per_eu, CAUSAL, PACKED>),
+  hipLaunchKernelGGL(
+      (attn_bwd_dkdv_kernel<D, sh.kb, sh.waves, sh.bm, sh.stages, sh.waves_per_eu, CAUSAL, PACKED, FUSED>),
                      dim3(n_units), dim3(64 * sh.waves), 0, a.stream, static_cast<const __bf16*>(a.q),
                      static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
                      static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dk),
-                     static_cast<__bf16*>(a.dv), static_cast<const __bf16*>(a.consts), units,
+                     static_cast<__bf16*>(a.dv), static_cast<__bf16*>(a.dq), static_cast<const __bf16*>(a.consts), units,
                      static_cast<const uint64_t*>(a.window_starts), n_units / kNumXcd, a.n_heads, a.total_tokens,
                      a.scale, a.scale * kLog2e);
   return hipGetLastError();
@@ -861,12 +955,15 @@ hipError_t launch_bwd_t(const BwdArgs& a) {
   if (a.n_units + a.n_wunits > 0) {
     if (ev.begin) (void)hipEventRecord(ev.begin, a.stream);
     if (a.n_units > 0) e = launch_dkdv_list<D, CAUSAL, false>(a, units, a.n_units);
-    if (e == hipSuccess && a.n_wunits > 0) e = launch_dkdv_list<D, CAUSAL, true>(a, units + a.n_units, a.n_wunits);
+    if (e == hipSuccess && a.n_wunits > 0)
+      e = launch_dkdv_list<D, CAUSAL, true, bwd_window_fused(D)>(a, units + a.n_units, a.n_wunits);
     if (ev.end) (void)hipEventRecord(ev.end, a.stream);
     if (e != hipSuccess) return e;
   }
   if (a.n_qunits > 0) e = launch_dq_list<D, CAUSAL, false>(a, qunits, a.n_qunits);
-  if (e == hipSuccess && a.n_wqunits > 0) e = launch_dq_list<D, CAUSAL, true>(a, qunits + a.n_qunits, a.n_wqunits);
+  // (windows with fused dQ: their dQ rows were written by the dK/dV pass)
+  if (e == hipSuccess && a.n_wqunits > 0 && !bwd_window_fused(D))
+    e = launch_dq_list<D, CAUSAL, true>(a, qunits + a.n_qunits, a.n_wqunits);
   return e;
 }
 

@@ -84,6 +84,18 @@ constexpr DkdvShape bwd_dkdv_window_shape(int head_dim) {
   return head_dim > 96 ? bwd_dkdv_shape(head_dim)
                        : DkdvShape{1, DCP_WIN_DKDV_WAVES, DCP_WIN_DKDV_BM, DCP_WIN_DKDV_STAGES, DCP_DKDV_WPE};
 }
+// Every query and key of a packed window lies inside the window, so at head
+// widths up to 96 one workgroup computes dQ of its window as well as dK and
+// dV (dS goes through LDS instead of being recomputed by the dQ pass), and
+// the dQ pass skips the windows.  This needs the two passes to cut the same
+// windows (equal window sizes).
+#ifndef DCP_WIN_FUSED
+#define DCP_WIN_FUSED 1
+#endif
+constexpr bool bwd_window_fused(int head_dim) {
+  return DCP_WIN_FUSED && head_dim <= 96 && DCP_WIN_DKDV_BM == 32 &&
+         32 * DCP_WIN_DKDV_WAVES == 32 * DCP_WIN_DQ_WAVES;
+}
 
 struct FwdArgs {
   const void* q;
