@@ -58,36 +58,54 @@ struct BwdShape {
 };
 
 // ---------------------------------------------------------------------------
-// 1. -Delta = -rowsum(dO o O) and LSE*log2e per (row, head), fp32 [H, T];
-// 16 lanes per (row, head), lane c covers columns 8c..8c+7.
+// 1. -Delta = -rowsum(dO o O) and LSE*log2e per (row, head), fp32 [H, T].
+// A workgroup takes kDeltaRows rows x up to kDeltaHeads heads: 16 lanes per
+// (row, head) pair, lane c covering columns 8c..8c+7.  Pairs are taken
+// row-major, so the heads of one token -- adjacent in memory -- are read
+// together and the bf16 rows arrive as whole cache lines; the sums meet in
+// LDS and leave head-major, kDeltaRows consecutive fp32 values (128 bytes)
+// per head.
+constexpr int kDeltaRows = 32, kDeltaHeads = 16;
 template <int D>
 __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict__ dout,
                                                         const __bf16* __restrict__ o,
                                                         const float* __restrict__ lse, float* __restrict__ ndelta,
                                                         float* __restrict__ lse2, int rows_end, int H, int T) {
   constexpr int CPR = D / 8;
-  const int64_t pair = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) >> 4;
+  constexpr int NPAIR = kDeltaRows * kDeltaHeads;
+  __shared__ float nd_lds[kDeltaHeads][kDeltaRows + 1];
+  const int r0 = blockIdx.x * kDeltaRows;
+  const int h0 = blockIdx.y * kDeltaHeads;
+  const int hc = min(kDeltaHeads, H - h0);
+  const int rows = min(kDeltaRows, rows_end - r0);
+  const int n_pairs = rows * hc;
   const int c = threadIdx.x & 15;
-  const int64_t n_pairs = int64_t(rows_end) * H;
-  float part = 0.f;
-  // pairs are head-major (pair = head * rows_end + row), so the fp32 [H, T]
-  // reads and writes of neighbouring lane groups are neighbouring rows
-  const int64_t row = pair % rows_end;
-  const int hh = int(pair / rows_end);
-  if (pair < n_pairs && c < CPR) {
-    const int64_t off = (row * H + hh) * D + 8 * c;
-    const bf16x8 a = *reinterpret_cast<const bf16x8*>(dout + off);
-    const bf16x8 b = *reinterpret_cast<const bf16x8*>(o + off);
+  // (every lane runs every step: the 16-lane reductions need all of them)
+#pragma unroll 8
+  for (int p = threadIdx.x >> 4; p < NPAIR; p += 16) {
+    const int r = p / hc, hh = p - r * hc;
+    float part = 0.f;
+    if (p < n_pairs && c < CPR) {
+      const int64_t off = (int64_t(r0 + r) * H + h0 + hh) * D + 8 * c;
+      const bf16x8 x = *reinterpret_cast<const bf16x8*>(dout + off);
+      const bf16x8 y = *reinterpret_cast<const bf16x8*>(o + off);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) part = fmaf(float(a[e]), float(b[e]), part);
+      for (int e = 0; e < 8; ++e) part = fmaf(float(x[e]), float(y[e]), part);
+    }
+    part += __shfl_xor(part, 8, 16);
+    part += __shfl_xor(part, 4, 16);
+    part += __shfl_xor(part, 2, 16);
+    part += __shfl_xor(part, 1, 16);
+    if (p < n_pairs && c == 0) nd_lds[hh][r] = -part;
   }
-  part += __shfl_xor(part, 8, 16);
-  part += __shfl_xor(part, 4, 16);
-  part += __shfl_xor(part, 2, 16);
-  part += __shfl_xor(part, 1, 16);
-  if (pair < n_pairs && c == 0) {
-    ndelta[int64_t(hh) * T + row] = -part;
-    lse2[int64_t(hh) * T + row] = lse[int64_t(hh) * T + row] * kLog2e;
+  __syncthreads();
+  for (int e = threadIdx.x; e < NPAIR; e += 256) {
+    const int hh = e / kDeltaRows, r = e % kDeltaRows;
+    if (hh < hc && r < rows) {
+      const int64_t i = int64_t(h0 + hh) * T + r0 + r;
+      ndelta[i] = nd_lds[hh][r];
+      lse2[i] = lse[i] * kLog2e;
+    }
   }
 }
 
@@ -939,10 +957,10 @@ hipError_t launch_dq_list(const BwdArgs& a, const WorkUnit* units, int n_units) 
 // and then its packed windows (one launch per non-empty list).
 template <int D, bool CAUSAL>
 hipError_t launch_bwd_t(const BwdArgs& a) {
-  const int64_t n_pairs = int64_t(a.rows_end) * a.n_heads;
-  if (n_pairs > 0) {
-    const int64_t blocks = (n_pairs * 16 + 255) / 256;
-    hipLaunchKernelGGL((bwd_delta_kernel<D>), dim3(unsigned(blocks)), dim3(256), 0, a.stream,
+  if (a.rows_end > 0) {
+    const dim3 grid(unsigned((a.rows_end + kDeltaRows - 1) / kDeltaRows),
+                    unsigned((a.n_heads + kDeltaHeads - 1) / kDeltaHeads));
+    hipLaunchKernelGGL((bwd_delta_kernel<D>), grid, dim3(256), 0, a.stream,
                        static_cast<const __bf16*>(a.dout), static_cast<const __bf16*>(a.o), a.lse, a.ndelta,
                        a.lse2, a.rows_end, a.n_heads, a.total_tokens);
     hipError_t e = hipGetLastError();
