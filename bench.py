@@ -188,14 +188,37 @@ def dkdv_bytes(cu, H: int, D: int) -> float:
     return 6.0 * rows * H * D * 2 + 2.0 * rows * H * 4
 
 
+def window_dq_part(P, cu, H: int, D: int, causal: bool):
+    """(rows, pairs) of the sequences the dK/dV pass runs as packed windows
+    when that launch also computes their dQ (the library does so up to head
+    width 96): their dQ rows are written, and their dQ products run, inside
+    the dK/dV pass."""
+    if D > 96:
+        return 0, 0
+    units, n_tiles, _ = P.work_list(cu, H, D, causal, 1)
+    win = units[n_tiles:]
+    win = win[(win[:, 4] == 0) & (win[:, 3] > 0)]
+    cu = np.asarray(cu, dtype=np.int64)
+    starts, lens = cu[:-1], np.diff(cu)
+    first = np.searchsorted(starts, win[:, 0], side="left")
+    last = np.searchsorted(starts, win[:, 0] + win[:, 3], side="left")
+    inside = np.zeros(lens.size, dtype=bool)
+    for a, b in zip(first, last):
+        inside[a:b] = True
+    inside &= lens > 0
+    return int(lens[inside].sum()), pairs_of(lens[inside].tolist(), causal)
+
+
 def roofline(flop: float, nbytes: float, ms: float, traffic) -> dict:
     """Roofline of the dK/dV pass: matrix-bound when its arithmetic
     intensity is above the ridge point (bf16 peak / HBM peak), else
     HBM-bound (short sequences: intensity grows with the sequence length)."""
     mfma = flop / nbytes >= BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
     out = {"kernel": "attn_bwd_dkdv_kernel", "flop_per_launch": flop, "bytes_per_launch": nbytes,
-           "flop_convention": "8*pairs*H*D (S, dP, dV, dK products)",
-           "bytes_convention": "6*rows*H*D*2 + 2*rows*H*4 (Q, K, V, dO, dK, dV; LSE, Delta)",
+           "flop_convention": "8*pairs*H*D (S, dP, dV, dK products) + 2*pairs*H*D over packed windows whose dQ "
+                              "the pass computes",
+           "bytes_convention": "6*rows*H*D*2 + 2*rows*H*4 (Q, K, V, dO, dK, dV; LSE, Delta) + rows*H*D*2 "
+                               "(dQ of those windows)",
            "traffic": traffic,
            "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)"}
     if mfma:
@@ -253,6 +276,7 @@ def main():
     value = (flop_fwd + flop_bwd) / (ms * 1e-3) / 1e12
     # the dK/dV pass forms S, dP, dV and dK: 4 of the 5 backward products
     flop_dkdv = 8.0 * pairs * H * D
+    win_rows, win_pairs = window_dq_part(P, cu, H, D, causal)
     dkdv_tflops = flop_dkdv / (bwd_ms * 1e-3) / 1e12
     fwd_tflops = flop_fwd / (fwd_ms * 1e-3) / 1e12
 
@@ -295,7 +319,8 @@ def main():
                    "flop_convention": "fwd 4*pairs*H*D + bwd 10*pairs*H*D"},
         "kernels": {"fwd_ms": fwd_ms, "fwd_tflops": fwd_tflops, "bwd_dkdv_ms": bwd_ms, "bwd_dkdv_tflops": dkdv_tflops,
                     "bwd_rest_ms": ms - fwd_ms - bwd_ms},
-        "roofline": roofline(flop_dkdv, dkdv_bytes(cu, H, D), bwd_ms, measured_traffic(args.workload)),
+        "roofline": roofline(flop_dkdv + 2.0 * win_pairs * H * D, dkdv_bytes(cu, H, D) + 2.0 * win_rows * H * D,
+                             bwd_ms, measured_traffic(args.workload)),
         "padded_baseline": padded,
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(w, args.seed),
     }

@@ -104,3 +104,17 @@ def test_tiny_config_and_edges():
     _check([0, 5], 2, 72, True, 1)  # one short sequence: a plain tile
     _check([0, 128, 256], 1, 128, False, 1)  # two sequences of exactly one dK/dV tile (D 128)
     _check(np.cumsum([0] + [1] * 600), 1, 72, False, 2)  # 600 one-token sequences
+
+
+def test_window_dq_accounting():
+    """The roofline's extra dQ work of packed windows (up to head width 96)
+    counts exactly the sequences the dK/dV list packs into windows."""
+    import bench as B
+    import paper_2608_07524_amd as P
+    cu = I.tiny().cu_seqlens  # 37 + 64 share a window; 128 and 200 run as tiles
+    assert B.window_dq_part(P, cu, 4, 64, False) == (101, 37 * 37 + 64 * 64)
+    assert B.window_dq_part(P, cu, 4, 64, True) == (101, 37 * 38 // 2 + 64 * 65 // 2)
+    assert B.window_dq_part(P, cu, 4, 128, False) == (0, 0)  # two-pass windows at head width 128
+    # windows {5, 0, 7} and {1, 1, 0}; 300 runs as tiles
+    cu = I.cu_from_lengths([5, 0, 7, 300, 1, 1, 0])
+    assert B.window_dq_part(P, cu, 2, 72, False) == (14, 25 + 49 + 1 + 1)
