@@ -213,7 +213,7 @@ __device__ __forceinline__ void to_mfma16_layout(bf16x8& xv, bf16x8& yv) {
 // and a copy of the window's K (both by transposing reads) from LDS.  To
 // fit two workgroups per CU the ring then holds Q and dO once, at the
 // row-read stride, and the transposing reads of dV and dK use that copy.
-template <int D, int KB, int NW, int BM, int NSTAGE, int WPE, bool CAUSAL, bool PACKED, bool FUSED>
+template <int D, int KB, int NW, int BM, int NSTAGE, int WPE, bool CAUSAL, bool PACKED, bool FUSED, bool ONECOPY>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) void attn_bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
@@ -223,14 +223,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   using S = BwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
   constexpr int RSTR = S::DP + 8;  // an odd number of 16-byte chunks
-  constexpr int TSTR = FUSED ? RSTR : S::TSTR;  // (fused: the one copy serves both reads)
+  constexpr int TSTR = ONECOPY ? RSTR : S::TSTR;  // (one copy: it serves both reads)
   static_assert(BM % 32 == 0, "whole 32-query blocks per tile");
-  static_assert(!FUSED || (PACKED && KB == 1 && BM == 32), "fused dQ: packed windows, 32-query tiles, KB 1");
+  static_assert(!FUSED || (PACKED && KB == 1 && BM == 32 && ONECOPY),
+                "fused dQ: packed windows, 32-query tiles, KB 1, one ring copy");
   using DR = DmaTile<BM, RSTR / 8, CPR, NW>;
   using DT = DmaTile<BM, TSTR / 8, CPR, NW>;
   using DL = DmaVecPair<BM, NW>;
-  constexpr int NI = FUSED ? 2 * DR::NI + DL::NI : 2 * DR::NI + 2 * DT::NI + DL::NI;  // copies per wavefront per tile
-  constexpr int RBUF = DR::ELEMS, TBUF = FUSED ? 0 : DT::ELEMS;
+  constexpr int NI = ONECOPY ? 2 * DR::NI + DL::NI : 2 * DR::NI + 2 * DT::NI + DL::NI;  // copies per wavefront per tile
+  constexpr int RBUF = DR::ELEMS, TBUF = ONECOPY ? 0 : DT::ELEMS;
   constexpr int SSTR = S::RSTR;  // epilogue staging stride
   // fused dQ: the window's K rows for transposing reads, and dS^T
   constexpr int NKEY = 32 * NW;
@@ -241,14 +242,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   constexpr int NMQ = (D + 15) / 16;            // 16-column blocks of dQ
   __shared__ __attribute__((aligned(16))) __bf16 Qr[NSTAGE * RBUF];
   __shared__ __attribute__((aligned(16))) __bf16 dOr[NSTAGE * RBUF];
-  __shared__ __attribute__((aligned(16))) __bf16 Qt[FUSED ? 8 : NSTAGE * TBUF];
-  __shared__ __attribute__((aligned(16))) __bf16 dOt[FUSED ? 8 : NSTAGE * TBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 Qt[ONECOPY ? 8 : NSTAGE * TBUF];
+  __shared__ __attribute__((aligned(16))) __bf16 dOt[ONECOPY ? 8 : NSTAGE * TBUF];
   __shared__ __attribute__((aligned(16))) float LV[NSTAGE * 2 * BM];  // LSE*log2e | -Delta
   __shared__ __attribute__((aligned(16))) __bf16 Kt[FUSED ? KTBUF : 8];
   __shared__ __attribute__((aligned(16))) __bf16 dSt[FUSED ? 2 * DSBUF : 8];
   constexpr int NSB = NW * KB;  // 32-key blocks per workgroup
   static_assert(NSB % 2 == 0 && NSTAGE * RBUF >= NSB / 2 * 32 * SSTR, "staging area too small");
-  static_assert(NSTAGE == 2 || NSTAGE == 3, "ring depth");
+  static_assert(NSTAGE >= 2 && NSTAGE <= 4, "ring depth");
+  static_assert(2 * NI < 64, "vmcnt range");
 
   const WorkUnit u = unit_for_block(units, per_xcd);
   if (u.rows == 0) return;
@@ -326,21 +328,23 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
     const __bf16* ds = doh + int64_t(q0) * ts;
     if (kFullCopies && valid >= BM) {
       DR::issue_full(&Qr[st * RBUF], qs, fo_r, wave);
-      if constexpr (!FUSED) DT::issue_full(&Qt[st * TBUF], qs, fo_t, wave);
+      if constexpr (!ONECOPY) DT::issue_full(&Qt[st * TBUF], qs, fo_t, wave);
       DR::issue_full(&dOr[st * RBUF], ds, fo_r, wave);
-      if constexpr (!FUSED) DT::issue_full(&dOt[st * TBUF], ds, fo_t, wave);
+      if constexpr (!ONECOPY) DT::issue_full(&dOt[st * TBUF], ds, fo_t, wave);
     } else {
       DR::issue(&Qr[st * RBUF], qs, ts, valid, zero, zero, wave, lane);
-      if constexpr (!FUSED) DT::issue(&Qt[st * TBUF], qs, ts, valid, zero, zero, wave, lane);
+      if constexpr (!ONECOPY) DT::issue(&Qt[st * TBUF], qs, ts, valid, zero, zero, wave, lane);
       DR::issue(&dOr[st * RBUF], ds, ts, valid, zero, zero, wave, lane);
-      if constexpr (!FUSED) DT::issue(&dOt[st * TBUF], ds, ts, valid, zero, zero, wave, lane);
+      if constexpr (!ONECOPY) DT::issue(&dOt[st * TBUF], ds, ts, valid, zero, zero, wave, lane);
     }
     // A query past the sequence end gets LSE = +inf, so its P is exactly 0.
     DL::issue(&LV[st * 2 * BM], lseh + q0, ndh + q0, valid, finf, fzero, wave, lane);
   };
-  // Waits until tile it+1 has landed (tile it+2 may stay in flight).
+  // Waits until tile it+1 has landed (the tiles after it may stay in flight).
   auto wait_next = [&](int it) DCP_INLINE {
-    if (NSTAGE == 3 && it + 2 < n_qt)
+    if (NSTAGE >= 4 && it + 3 < n_qt)
+      wait_vmcnt<2 * NI>();
+    else if (NSTAGE >= 3 && it + 2 < n_qt)
       wait_vmcnt<NI>();
     else
       wait_vmcnt<0>();
@@ -364,8 +368,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
 #pragma unroll
       for (int nb = 0; nb < NMB; ++nb) dk16[kb][mb][nb] = dv16[kb][mb][nb] = f32x4{};
 
-  issue_tile(0);
-  if (NSTAGE == 3 && n_qt > 1) issue_tile(1);
+  for (int i = 0; i < NSTAGE - 1 && i < n_qt; ++i) issue_tile(i);
   wait_next(-1);
   __syncthreads();
 
@@ -381,10 +384,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
               : (4 * g + ((lane & 15) >> 2)) * TSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const lds_bf16* Qr3 = lds_ptr(Qr);
   const lds_bf16* dOr3 = lds_ptr(dOr);
-  const lds_bf16* Qt3 = FUSED ? Qr3 : lds_ptr(Qt);
-  const lds_bf16* dOt3 = FUSED ? dOr3 : lds_ptr(dOt);
+  const lds_bf16* Qt3 = ONECOPY ? Qr3 : lds_ptr(Qt);
+  const lds_bf16* dOt3 = ONECOPY ? dOr3 : lds_ptr(dOt);
   const lds_f32* LV3 = lds_ptr(LV);
-  constexpr unsigned TBUF_R = FUSED ? RBUF : TBUF;  // stage size of the transposing-read copies
+  constexpr unsigned TBUF_R = ONECOPY ? RBUF : TBUF;  // stage size of the transposing-read copies
 
   // (fused) this lane's four 8-byte slots of the dS^T buffer of tile it:
   // key 32*wave + j, queries 8b + 4g .. +3 for b = 0..3 at bf16x4 index 2b
@@ -931,7 +934,8 @@ template <int D, bool CAUSAL, bool PACKED, bool FUSED = false>
 hipError_t launch_dkdv_list(const BwdArgs& a, const WorkUnit* units, int n_units) {
   constexpr DkdvShape sh = PACKED ? bwd_dkdv_window_shape(D) : bwd_dkdv_shape(D);
   hipLaunchKernelGGL(
-      (attn_bwd_dkdv_kernel<D, sh.kb, sh.waves, sh.bm, sh.stages, sh.waves_per_eu, CAUSAL, PACKED, FUSED>),
+      (attn_bwd_dkdv_kernel<D, sh.kb, sh.waves, sh.bm, sh.stages, sh.waves_per_eu, CAUSAL, PACKED, FUSED,
+                            FUSED || sh.onecopy>),
                      dim3(n_units), dim3(64 * sh.waves), 0, a.stream, static_cast<const __bf16*>(a.q),
                      static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
                      static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dk),

@@ -15,13 +15,18 @@ constexpr int kFwdWaves = DCP_FWD_WAVES;
 // 32*kb keys whose K, V fragments and dK, dV accumulators stay resident,
 // stepping over `bm` queries at a time through a `stages`-deep LDS ring;
 // waves_per_eu is the occupancy the register allocation must allow.
-// Head widths up to 72 run two wavefronts of 32 keys per SIMD.  At head
-// width 128 the resident state needs more than the 256 registers two
-// wavefronts per SIMD could each have, so that width runs one wavefront per
-// SIMD, and its ring holds two stages (three do not fit the 160 KB of LDS).
+// Head widths up to 72 run two wavefronts of 32 keys per SIMD, with Q and
+// dO held once per ring stage (the transposing reads of dV and dK use the
+// row-read copy, at the cost of some bank conflicts), which leaves LDS for
+// a four-stage ring of 64-query tiles.  At head width 128 the resident
+// state needs more than the 256 registers two wavefronts per SIMD could
+// each have, so that width runs one wavefront per SIMD; its ring holds Q
+// and dO once too, in two stages of 128-query tiles (139 KB of the 160 KB
+// of LDS), so that a barrier comes every four 32-query blocks.
 // dQ pass: kBwdDqWaves wavefronts of 32 queries, kBwdDqBN keys per step.
 struct DkdvShape {
   int kb, waves, bm, stages, waves_per_eu;
+  bool onecopy;  // the ring holds Q and dO once (row-read stride) instead of twice
 };
 #ifndef DCP_DKDV_KB
 #define DCP_DKDV_KB 1
@@ -35,18 +40,35 @@ struct DkdvShape {
 #ifndef DCP_DKDV_WPE
 #define DCP_DKDV_WPE 2
 #endif
+#ifndef DCP_DKDV_STAGES
+#define DCP_DKDV_STAGES 4
+#endif
+#ifndef DCP_DKDV_ONECOPY
+#define DCP_DKDV_ONECOPY 1
+#endif
 #ifndef DCP_DKDV_KB_D128
 #define DCP_DKDV_KB_D128 1
 #endif
 #ifndef DCP_DKDV_WAVES_D128
 #define DCP_DKDV_WAVES_D128 4
 #endif
+#ifndef DCP_DKDV_BM_D128
+#define DCP_DKDV_BM_D128 128
+#endif
+#ifndef DCP_DKDV_STAGES_D128
+#define DCP_DKDV_STAGES_D128 2
+#endif
+#ifndef DCP_DKDV_ONECOPY_D128
+#define DCP_DKDV_ONECOPY_D128 1
+#endif
 #ifndef DCP_BWD_DQ_WAVES
 #define DCP_BWD_DQ_WAVES 8
 #endif
 constexpr DkdvShape bwd_dkdv_shape(int head_dim) {
-  return head_dim > 96 ? DkdvShape{DCP_DKDV_KB_D128, DCP_DKDV_WAVES_D128, 64, 2, 1}
-                       : DkdvShape{DCP_DKDV_KB, DCP_DKDV_WAVES, DCP_DKDV_BM, 3, DCP_DKDV_WPE};
+  return head_dim > 96 ? DkdvShape{DCP_DKDV_KB_D128, DCP_DKDV_WAVES_D128, DCP_DKDV_BM_D128, DCP_DKDV_STAGES_D128, 1,
+                                   DCP_DKDV_ONECOPY_D128 != 0}
+                       : DkdvShape{DCP_DKDV_KB, DCP_DKDV_WAVES, DCP_DKDV_BM, DCP_DKDV_STAGES, DCP_DKDV_WPE,
+                                   DCP_DKDV_ONECOPY != 0};
 }
 constexpr int kBwdDqWaves = DCP_BWD_DQ_WAVES;
 constexpr int kBwdDqBN = 64;
@@ -82,7 +104,7 @@ constexpr int kWinDqWaves = DCP_WIN_DQ_WAVES;
 constexpr int kWinDqStages = DCP_WIN_DQ_STAGES;
 constexpr DkdvShape bwd_dkdv_window_shape(int head_dim) {
   return head_dim > 96 ? bwd_dkdv_shape(head_dim)
-                       : DkdvShape{1, DCP_WIN_DKDV_WAVES, DCP_WIN_DKDV_BM, DCP_WIN_DKDV_STAGES, DCP_DKDV_WPE};
+                       : DkdvShape{1, DCP_WIN_DKDV_WAVES, DCP_WIN_DKDV_BM, DCP_WIN_DKDV_STAGES, DCP_DKDV_WPE, false};
 }
 // Every query and key of a packed window lies inside the window, so at head
 // widths up to 96 one workgroup computes dQ of its window as well as dK and
