@@ -657,8 +657,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
 // LSE*log2e and -Delta in registers while key tiles of BN rows stream
 // through an NSTAGE-deep LDS ring filled by direct global-to-LDS copies
 // NSTAGE - 1 tiles ahead (K twice: rows read 16 B per lane for S^T, rows
-// read by transposing reads for dQ^T; V once), one barrier per tile.
-template <int D, int NW, int NSTAGE, bool CAUSAL, bool PACKED>
+// read by transposing reads for dQ^T; V once), one barrier per tile.  With
+// ONECOPY, K is held once, at the row-read stride, and the transposing
+// reads use that copy.
+template <int D, int NW, int NSTAGE, bool CAUSAL, bool PACKED, bool ONECOPY>
 __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
@@ -667,17 +669,18 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   using S = BwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
   constexpr int KSTR = S::DP + 8;  // K and V rows read 16 B per lane
-  constexpr int TSTR = S::TSTR;    // second copy of K for transposing reads
+  constexpr int TSTR = ONECOPY ? KSTR : S::TSTR;  // (second copy of K for transposing reads)
   constexpr int BN = kBwdDqBN;
-  constexpr int KBUF = BN * KSTR, TBUF = BN * TSTR;
+  constexpr int KBUF = BN * KSTR, TBUF = ONECOPY ? 0 : BN * TSTR;
   using DK = DmaTile<BN, KSTR / 8, CPR, NW>;
   using DT = DmaTile<BN, TSTR / 8, CPR, NW>;
-  constexpr int NI = 2 * DK::NI + DT::NI;  // copies per wavefront per tile
+  constexpr int NI = ONECOPY ? 2 * DK::NI : 2 * DK::NI + DT::NI;  // copies per wavefront per tile
 
   __shared__ __attribute__((aligned(16))) __bf16 Ks[NSTAGE * KBUF];
   __shared__ __attribute__((aligned(16))) __bf16 Vs[NSTAGE * KBUF];
-  __shared__ __attribute__((aligned(16))) __bf16 Kt[NSTAGE * TBUF];
-  static_assert(NSTAGE == 2 || NSTAGE == 3, "ring depth");
+  __shared__ __attribute__((aligned(16))) __bf16 Kt[ONECOPY ? 8 : NSTAGE * TBUF];
+  static_assert(NSTAGE >= 2 && NSTAGE <= 4, "ring depth");
+  static_assert(2 * NI < 64, "vmcnt range");
 
   const WorkUnit u = unit_for_block(units, per_xcd);
   if (u.rows == 0) return;
@@ -742,18 +745,19 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
     if (valid >= BN) {
       DK::issue_full(&Ks[st * KBUF], ks, fo_k, wave);
       DK::issue_full(&Vs[st * KBUF], vh + int64_t(kt) * BN * ts, fo_k, wave);
-      DT::issue_full(&Kt[st * TBUF], ks, fo_t, wave);
+      if constexpr (!ONECOPY) DT::issue_full(&Kt[st * TBUF], ks, fo_t, wave);
     } else {
       DK::issue(&Ks[st * KBUF], ks, ts, valid, zero, zero, wave, lane);
       DK::issue(&Vs[st * KBUF], vh + int64_t(kt) * BN * ts, ts, valid, zero, zero, wave, lane);
-      DT::issue(&Kt[st * TBUF], ks, ts, valid, zero, zero, wave, lane);
+      if constexpr (!ONECOPY) DT::issue(&Kt[st * TBUF], ks, ts, valid, zero, zero, wave, lane);
     }
   };
-  // Before the barrier that ends tile kt: tile kt+1 must have landed; only
-  // tile kt+2's copies (three stages: issued this iteration) may still be
-  // in flight.
+  // Before the barrier that ends tile kt: tile kt+1 must have landed; the
+  // later tiles' copies may still be in flight.
   auto wait_next = [&](int kt) DCP_INLINE {
-    if (NSTAGE == 3 && kt + 2 < n_tiles)
+    if (NSTAGE >= 4 && kt + 3 < n_tiles)
+      wait_vmcnt<2 * NI>();
+    else if (NSTAGE >= 3 && kt + 2 < n_tiles)
       wait_vmcnt<NI>();
     else
       wait_vmcnt<0>();
@@ -769,8 +773,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
 #pragma unroll
   for (int mb = 0; mb < NMB; ++mb) acc16[mb][0] = acc16[mb][1] = f32x4{};
 
-  if (n_tiles > 0) issue_tile(0);
-  if (NSTAGE == 3 && n_tiles > 1) issue_tile(1);
+  for (int i = 0; i < NSTAGE - 1 && i < n_tiles; ++i) issue_tile(i);
   wait_next(-1);
   __syncthreads();
 
@@ -783,7 +786,8 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
               : (4 * g + ((lane & 15) >> 2)) * TSTR + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const lds_bf16* Ks3 = lds_ptr(Ks);
   const lds_bf16* Vs3 = lds_ptr(Vs);
-  const lds_bf16* Kt3 = lds_ptr(Kt);
+  const lds_bf16* Kt3 = ONECOPY ? Ks3 : lds_ptr(Kt);
+  constexpr unsigned TBUF_R = ONECOPY ? KBUF : TBUF;  // stage size of the transposing-read copy
   const int wave_last_q = wave_q0 + 31;
 
   // One key tile against this wavefront's 32 queries.  MASK covers tiles
@@ -791,7 +795,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
   auto process_tile = [&](unsigned st, int k0, auto mask_tag) DCP_INLINE {
     constexpr bool MASK = decltype(mask_tag)::value;
     unsigned rb = st * KBUF + ar_off;
-    unsigned tb = st * TBUF + tr_off;
+    unsigned tb = st * TBUF_R + tr_off;
     asm("" : "+v"(rb), "+v"(tb));  // keeps the constant terms in the offset fields
     f32x16 s[BN / 32], dp[BN / 32];
 #pragma unroll
@@ -948,8 +952,8 @@ hipError_t launch_dkdv_list(const BwdArgs& a, const WorkUnit* units, int n_units
 template <int D, bool CAUSAL, bool PACKED>
 hipError_t launch_dq_list(const BwdArgs& a, const WorkUnit* units, int n_units) {
   constexpr int NW = PACKED ? kWinDqWaves : kBwdDqWaves;
-  constexpr int NS = D > 96 ? 2 : (PACKED ? kWinDqStages : 3);
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NW, NS, CAUSAL, PACKED>), dim3(n_units), dim3(64 * NW), 0, a.stream, static_cast<const __bf16*>(a.q),
+  constexpr int NS = D > 96 ? kBwdDqStagesD128 : (PACKED ? kWinDqStages : kBwdDqStages);
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NW, NS, CAUSAL, PACKED, kBwdDqOneCopy>), dim3(n_units), dim3(64 * NW), 0, a.stream, static_cast<const __bf16*>(a.q),
                      static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
                      static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dq),
                      static_cast<const __bf16*>(a.consts), units, static_cast<const uint64_t*>(a.qwindow_starts),

@@ -23,7 +23,10 @@ constexpr int kFwdWaves = DCP_FWD_WAVES;
 // each have, so that width runs one wavefront per SIMD; its ring holds Q
 // and dO once too, in two stages of 128-query tiles (139 KB of the 160 KB
 // of LDS), so that a barrier comes every four 32-query blocks.
-// dQ pass: kBwdDqWaves wavefronts of 32 queries, kBwdDqBN keys per step.
+// dQ pass: kBwdDqWaves wavefronts of 32 queries, kBwdDqBN keys per step,
+// K held once per ring stage (its transposing reads share the row-read
+// copy; at head width 128 this also frees the registers the second copy's
+// offsets took).
 struct DkdvShape {
   int kb, waves, bm, stages, waves_per_eu;
   bool onecopy;  // the ring holds Q and dO once (row-read stride) instead of twice
@@ -72,6 +75,18 @@ constexpr DkdvShape bwd_dkdv_shape(int head_dim) {
 }
 constexpr int kBwdDqWaves = DCP_BWD_DQ_WAVES;
 constexpr int kBwdDqBN = 64;
+#ifndef DCP_BWD_DQ_STAGES
+#define DCP_BWD_DQ_STAGES 3
+#endif
+#ifndef DCP_BWD_DQ_STAGES_D128
+#define DCP_BWD_DQ_STAGES_D128 2
+#endif
+#ifndef DCP_BWD_DQ_ONECOPY
+#define DCP_BWD_DQ_ONECOPY 1
+#endif
+constexpr int kBwdDqStages = DCP_BWD_DQ_STAGES;
+constexpr int kBwdDqStagesD128 = DCP_BWD_DQ_STAGES_D128;
+constexpr bool kBwdDqOneCopy = DCP_BWD_DQ_ONECOPY != 0;
 
 // Packed windows (runs of short sequences sharing one tile) launch with
 // their own shape: fewer wavefronts per workgroup (smaller tiles) and a
