@@ -38,6 +38,10 @@
 namespace dcp {
 namespace {
 
+#ifndef DCP_BWD_OSTR
+#define DCP_BWD_OSTR 1  // 0: one-copy tiles at the minimal row-read stride
+#endif
+
 template <int D>
 struct BwdShape {
   static constexpr int DP = (D + 15) / 16 * 16;  // contraction width (zero padded)
@@ -55,6 +59,17 @@ struct BwdShape {
   // fewer padded columns than 32-column blocks (D = 72: 80 instead of 96).
   static constexpr int NMB = (D + 15) / 16;
   static constexpr bool KV16 = NMB * 16 < NDB * 32;
+  // Stride of a tile held once and read both ways.  An odd number of
+  // 16-byte chunks keeps the 16-byte row reads conflict-free (16 lanes, 16
+  // rows: 64 banks).  The transposing reads of a half-wavefront cover 4
+  // consecutive rows (KV16: 8 bank-wide runs of 32 bytes; else 16-bank runs
+  // of 64 bytes), so the row starts should spread over the banks: at D = 72,
+  // 104 elements puts them 12 banks apart and every run lands on its own
+  // banks (only the two row groups 16 apart, always on the same banks,
+  // meet); at D = 128, 152 elements leaves two-way overlaps where the
+  // minimal 136 stacks four.
+  static constexpr int OSTR = !DCP_BWD_OSTR ? DP + 8 : D == 72 ? 104 : D == 128 ? 152 : DP + 8;
+  static_assert(OSTR % 16 == 8 && OSTR >= (KV16 ? NMB * 16 : NDB * 32), "one-copy stride");
 };
 
 // ---------------------------------------------------------------------------
@@ -222,7 +237,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
     float scale, float scale_log2) {
   using S = BwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
-  constexpr int RSTR = S::DP + 8;  // an odd number of 16-byte chunks
+  // an odd number of 16-byte chunks (one copy outside packed windows: the
+  // stride that also spreads the transposing reads; the fused window launch
+  // keeps the minimal one to fit two workgroups per CU)
+  constexpr int RSTR = (ONECOPY && !FUSED) ? S::OSTR : S::DP + 8;
   constexpr int TSTR = ONECOPY ? RSTR : S::TSTR;  // (one copy: it serves both reads)
   static_assert(BM % 32 == 0, "whole 32-query blocks per tile");
   static_assert(!FUSED || (PACKED && KB == 1 && BM == 32 && ONECOPY),
@@ -668,7 +686,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
     const uint64_t* __restrict__ window_starts, int per_xcd, int H, int T, float scale, float scale_log2) {
   using S = BwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, CPR = S::CPR;
-  constexpr int KSTR = S::DP + 8;  // K and V rows read 16 B per lane
+  constexpr int KSTR = ONECOPY ? S::OSTR : S::DP + 8;  // K and V rows read 16 B per lane (and K transposed)
   constexpr int TSTR = ONECOPY ? KSTR : S::TSTR;  // (second copy of K for transposing reads)
   constexpr int BN = kBwdDqBN;
   constexpr int KBUF = BN * KSTR, TBUF = ONECOPY ? 0 : BN * TSTR;
