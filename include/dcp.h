@@ -115,7 +115,11 @@ int dcp_varlen_attn_fwd(const dcp_attn_desc* desc, const void* q, const void* k,
  *   q, k, v       the forward's inputs.
  *   dq, dk, dv    bf16 [T, H, D] outputs (rows of sequences only).
  *   workspace     device scratch of at least the queried size; it holds the
- *                 fp32 dQ accumulator and rowsum(dO o O).
+ *                 work lists, -rowsum(dO o O) and LSE * log2(e) (fp32 [H, T]
+ *                 each).  There is no dQ accumulator: dQ is formed by
+ *                 query-stationary workgroups (or, for packed windows at head
+ *                 widths up to 96, by the window's dK/dV workgroup), so every
+ *                 gradient is written once and is bitwise reproducible.
  * The call uses the same desc (scale, causal) as the forward.
  */
 int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, const void* o, const float* lse,
@@ -125,7 +129,9 @@ int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, const void*
 /*
  * The work the attention kernels run for `desc` (introspection for
  * schedulers and tests: launches nothing, needs no GPU).  pass 0 is the
- * forward, 1 the dK/dV pass, 2 the dQ pass.  Each unit is 5 int32
+ * forward, 1 the dK/dV pass, 2 the dQ pass (at head widths up to 96 the dQ
+ * pass launches only its sequence tiles: the dK/dV launch over the same
+ * packed windows forms their dQ too).  Each unit is 5 int32
  * {row0, seq0, seqlen, rows, head}: rows [row0, row0 + rows) of head `head`
  * in the sequence occupying rows [seq0, seq0 + seqlen); rows == 0 is
  * padding.  Units [0, *n_tiles) are such sequence tiles (tiles restart at
@@ -150,10 +156,10 @@ int dcp_work_list(const dcp_attn_desc* desc, int32_t pass, int32_t* units, size_
  * Instrumentation hook for profilers and benchmarks.  begin/end are
  * hipEvent_t handles (as void*) created by the caller.  While set on the
  * calling thread, every dcp_varlen_attn_fwd call records `begin` right
- * before its attention kernel and `end` right after it, and every
- * dcp_varlen_attn_bwd call does the same around its main kernel (the one
- * forming dQ, dK, dV), on the call's stream; the small pre/post passes and
- * the work-list upload fall outside the pair.  Passing NULL, NULL clears the
+ * before its attention kernel and `end` right after it (its sequence-tile
+ * and packed-window launches), and every dcp_varlen_attn_bwd call does the
+ * same around its dK/dV pass, on the call's stream; the Delta and dQ passes
+ * and the work-list upload fall outside the pair.  Passing NULL, NULL clears the
  * hook.  Costs two event records per call while set, nothing otherwise.
  */
 int dcp_set_kernel_events(void* begin, void* end);
