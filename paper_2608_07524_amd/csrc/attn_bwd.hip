@@ -79,10 +79,12 @@ struct BwdShape {
 // row-major, so the heads of one token -- adjacent in memory -- are read
 // together and the bf16 rows arrive as whole cache lines; the sums meet in
 // LDS and leave head-major, kDeltaRows consecutive fp32 values (128 bytes)
-// per head.
-constexpr int kDeltaRows = 32, kDeltaHeads = 16;
+// per head.  1024 threads: each 16-lane group takes 8 pairs, all loads in
+// flight at once (short sequences give few workgroups, so the per-workgroup
+// latency is the pass's).
+constexpr int kDeltaRows = 32, kDeltaHeads = 16, kDeltaThreads = 1024;
 template <int D>
-__global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict__ dout,
+__global__ __launch_bounds__(kDeltaThreads) void bwd_delta_kernel(const __bf16* __restrict__ dout,
                                                         const __bf16* __restrict__ o,
                                                         const float* __restrict__ lse, float* __restrict__ ndelta,
                                                         float* __restrict__ lse2, int rows_end, int H, int T) {
@@ -96,8 +98,8 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict
   const int n_pairs = rows * hc;
   const int c = threadIdx.x & 15;
   // (every lane runs every step: the 16-lane reductions need all of them)
-#pragma unroll 8
-  for (int p = threadIdx.x >> 4; p < NPAIR; p += 16) {
+#pragma unroll
+  for (int p = threadIdx.x >> 4; p < NPAIR; p += kDeltaThreads / 16) {
     const int r = p / hc, hh = p - r * hc;
     float part = 0.f;
     if (p < n_pairs && c < CPR) {
@@ -114,7 +116,7 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict
     if (p < n_pairs && c == 0) nd_lds[hh][r] = -part;
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < NPAIR; e += 256) {
+  for (int e = threadIdx.x; e < NPAIR; e += kDeltaThreads) {
     const int hh = e / kDeltaRows, r = e % kDeltaRows;
     if (hh < hc && r < rows) {
       const int64_t i = int64_t(h0 + hh) * T + r0 + r;
@@ -986,7 +988,7 @@ hipError_t launch_bwd_t(const BwdArgs& a) {
   if (a.rows_end > 0) {
     const dim3 grid(unsigned((a.rows_end + kDeltaRows - 1) / kDeltaRows),
                     unsigned((a.n_heads + kDeltaHeads - 1) / kDeltaHeads));
-    hipLaunchKernelGGL((bwd_delta_kernel<D>), grid, dim3(256), 0, a.stream,
+    hipLaunchKernelGGL((bwd_delta_kernel<D>), grid, dim3(kDeltaThreads), 0, a.stream,
                        static_cast<const __bf16*>(a.dout), static_cast<const __bf16*>(a.o), a.lse, a.ndelta,
                        a.lse2, a.rows_end, a.n_heads, a.total_tokens);
     hipError_t e = hipGetLastError();
