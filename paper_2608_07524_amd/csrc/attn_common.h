@@ -162,19 +162,26 @@ __device__ __forceinline__ void wait_vmcnt() {
 // rows r < valid_rows come from src + r*row_stride + 8c, slot c == CPR_DATA
 // from `first_pad` (a 16-byte constant chunk, e.g. [1, 0, ..., 0] for a
 // row-sum column) and every other slot from `zero`.  The tile occupies
-// ELEMS = 512*NINS elements: when ROWS*CPR_PAD is not a multiple of 64,
+// ELEMS = 512*NINS elements (plus the group skews below): when ROWS*CPR_PAD is not a multiple of 64,
 // the last copy also fills the slots past the tile with zeros.  Every
 // wavefront issues exactly NI instructions per tile (the last one repeated
 // when they do not split evenly; the repeat rewrites identical bytes), so
 // a fixed wait_vmcnt count covers the tile on every wavefront.  Completion
 // is tracked by vmcnt only: wait, then barrier, before reading the tile.
-template <int ROWS, int CPR_PAD, int CPR_DATA, int NW>
+// GSKEW > 0 starts every 16-row group of the tile GSKEW elements further
+// on (row r at element r * 8 * CPR_PAD + GSKEW * (r / 16)): a group is a
+// whole number of copies, so only the copies' LDS bases move.
+template <int ROWS, int CPR_PAD, int CPR_DATA, int NW, int GSKEW = 0>
 struct DmaTile {
   static constexpr int NSLOT = ROWS * CPR_PAD;
   static constexpr int NINS = (NSLOT + 63) / 64;
   static constexpr int NI = (NINS + NW - 1) / NW;
-  static constexpr int ELEMS = 512 * NINS;
+  static constexpr int IPG = GSKEW ? 16 * CPR_PAD / 64 : 1;  // copies per 16-row group
+  static_assert(GSKEW == 0 || (16 * CPR_PAD % 64 == 0 && ROWS % 16 == 0), "skewed groups are whole copies");
+  static constexpr int ELEMS = 512 * NINS + GSKEW * (NINS / IPG);
   static_assert(CPR_DATA < CPR_PAD, "pad slots hold the constant chunks");
+  // element offset of copy t inside the tile
+  __device__ __forceinline__ static constexpr int dst(int t) { return 512 * t + GSKEW * (t / IPG); }
 
   __device__ __forceinline__ static void issue(__bf16* lds_tile, const __bf16* src, int64_t row_stride,
                                                int valid_rows, const __bf16* zero, const __bf16* first_pad,
@@ -190,7 +197,7 @@ struct DmaTile {
       } else if (c == CPR_DATA && r < ROWS) {
         g = first_pad;
       }
-      dma16(g, lds_tile + 512 * t);
+      dma16(g, lds_tile + dst(t));
     }
   }
 
@@ -230,7 +237,7 @@ struct DmaTile {
     for (int i = 0; i < NI; ++i) {
       const int t = min(wave + NW * i, NINS - 1);
       const uint32_t m0 = __builtin_amdgcn_readfirstlane(
-          static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds_tile + 512 * t)));
+          static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds_tile + dst(t))));
       asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
                    :
                    : "s"(m0), "v"(fo.off[i]), "s"(base)
@@ -266,7 +273,7 @@ struct DmaTile {
     for (int i = 0; i < NI; ++i) {
       const int t = min(wave + NW * i, NINS - 1);
       const uint32_t m0 = __builtin_amdgcn_readfirstlane(
-          static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds_tile + 512 * t)));
+          static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds_tile + dst(t))));
       uint64_t saved;
       asm volatile(
           "s_mov_b64 %0, exec\n\t"

@@ -47,6 +47,10 @@ static_assert(kFwdStages >= 3 && kWinFwdStages >= 3, "tiles kt and kt + 1 are re
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 constexpr float kNoMax = -1e30f;       // running max before any key
 
+#ifndef DCP_FWD_VSKEW
+#define DCP_FWD_VSKEW 1
+#endif
+
 template <int D>
 struct FwdShape {
   static constexpr int DP = (D + 15) / 16 * 16;  // contraction width (zero padded)
@@ -65,6 +69,12 @@ struct FwdShape {
   // from 16x16x32 products instead.
   static constexpr int NMB = (D + 1 + 15) / 16;
   static constexpr bool PV16 = ONES_ROW && NMB * 16 < NDB * 32;
+  // With 16x16x32 products a half-wavefront's transposing reads cover rows
+  // 0..3 and 16..19 of a 32-key block, which any row stride puts on the
+  // same banks (16 rows x 64 mod 128 bytes = 0 mod 256); starting every
+  // 16-row group of the V tile 32 bytes further on moves the second set of
+  // rows onto the other half of each bank run.
+  static constexpr int VSKEW = (PV16 && DCP_FWD_VSKEW) ? 16 : 0;
 };
 
 // Interleaving hints for the compiler's scheduler (masks of
@@ -91,12 +101,13 @@ __global__ __launch_bounds__(64 * NW) DCP_FWD_OCCUPANCY void attn_fwd_kernel(con
   using S = FwdShape<D>;
   constexpr int NKD = S::NKD, NDB = S::NDB, KSTR = S::KSTR, VSTR = S::VSTR, CPR = S::CPR;
   constexpr int BN = kFwdBN;
-  constexpr int KBUF = BN * KSTR, VBUF = BN * VSTR;
+  constexpr int KBUF = BN * KSTR;
+  using DK = DmaTile<BN, KSTR / 8, CPR, NW>;
+  using DV = DmaTile<BN, VSTR / 8, CPR, NW, S::VSKEW>;
+  constexpr int VBUF = DV::ELEMS;
   // as deep as asked, within the 160 KB of LDS
   constexpr int NST = STAGES * 2 * (KBUF + VBUF) <= 163840 ? STAGES : 163840 / (2 * (KBUF + VBUF));
   static_assert(NST >= 3, "ring too shallow");
-  using DK = DmaTile<BN, KSTR / 8, CPR, NW>;
-  using DV = DmaTile<BN, VSTR / 8, CPR, NW>;
   constexpr int NI = DK::NI + DV::NI;  // copies per wavefront per tile
 
   __shared__ __attribute__((aligned(16))) __bf16 Ks[NST * KBUF];
@@ -180,7 +191,7 @@ __global__ __launch_bounds__(64 * NW) DCP_FWD_OCCUPANCY void attn_fwd_kernel(con
   if constexpr (S::ONES_ROW) {
     for (int idx = tid; idx < NST * BN; idx += 64 * NW) {
       const int st = idx / BN, r = idx % BN;
-      *reinterpret_cast<bf16x8*>(&Vs[st * VBUF + r * VSTR + 8 * CPR]) =
+      *reinterpret_cast<bf16x8*>(&Vs[st * VBUF + r * VSTR + S::VSKEW * (r / 16) + 8 * CPR]) =
           bf16x8{__bf16(1.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f)};
     }
   }
@@ -220,7 +231,8 @@ __global__ __launch_bounds__(64 * NW) DCP_FWD_OCCUPANCY void attn_fwd_kernel(con
   // (16x16x32 products: lane group g4 = lane / 16 reads the key runs
   // starting at 0, 16, 4, 20 and 8 further, see pv_product)
   const int g4 = lane >> 4;
-  const unsigned tr16_off = (16 * (g4 & 1) + 4 * (g4 >> 1) + ((lane & 15) >> 2)) * VSTR + 4 * (lane & 3);
+  const unsigned tr16_off =
+      (16 * (g4 & 1) + 4 * (g4 >> 1) + ((lane & 15) >> 2)) * VSTR + S::VSKEW * (g4 & 1) + 4 * (lane & 3);
   const unsigned tr_lane = S::PV16 ? tr16_off : tr_off;
   // and the 16-byte read offset inside a K tile
   const unsigned kr_off = j * KSTR + 8 * g;
@@ -401,7 +413,7 @@ __global__ __launch_bounds__(64 * NW) DCP_FWD_OCCUPANCY void attn_fwd_kernel(con
     unsigned vb0 = (unsigned(kt) % NST) * VBUF + tr_lane;
     asm("" : "+v"(kb0), "+v"(kb1), "+v"(vb0));  // keeps the constant terms in the offset fields
     step(2 * kt + 1, kb0 + 32 * KSTR, vb0, 2 * kt + 1 < 2 * t_work, mask_tag);
-    step(2 * kt + 2, kb1, vb0 + 32 * VSTR, 2 * kt + 2 < 2 * t_work, mask_tag);
+    step(2 * kt + 2, kb1, vb0 + 32 * VSTR + 2 * S::VSKEW, 2 * kt + 2 < 2 * t_work, mask_tag);
     wait_for(kt + 1);
     __syncthreads();
   };
