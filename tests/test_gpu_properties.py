@@ -36,10 +36,13 @@ def _outputs(torch, bits, cu, scale, causal):
     return [to_bits(o), lse.cpu().numpy(), to_bits(dq), to_bits(dk), to_bits(dv)]
 
 
-@pytest.mark.parametrize("D,causal", [(72, False), (128, True)])
-def test_bitwise_deterministic(torch, D, causal):
+# (the last two cases run packed windows: at head widths up to 96 their dQ
+# comes from the window's dK/dV workgroup through LDS, still without atomics)
+@pytest.mark.parametrize("D,causal,lengths", [(72, False, [700, 1, 2049, 300]), (128, True, [700, 1, 2049, 300]),
+                                              (72, False, [5, 17, 40, 3, 700, 60, 60, 1, 0, 9, 127]),
+                                              (64, True, [5, 17, 40, 3, 700, 60, 60, 1, 0, 9, 127])])
+def test_bitwise_deterministic(torch, D, causal, lengths):
     rng = np.random.default_rng(7)
-    lengths = [700, 1, 2049, 300]
     cu = I.cu_from_lengths(lengths)
     bits = I.tensors(rng, int(cu[-1]), 4, D)
     a = _outputs(torch, bits, cu, 1 / math.sqrt(D), causal)
