@@ -192,6 +192,25 @@ def test_text_causal_pack(torch):
     _check_identities(q, v, do, out, w, "text causal")
 
 
+def test_transformer_1d_causal_pack(torch):
+    """The Transformer-1D layer's attention shape (Sec. 4.1: hidden 3072 as
+    48 heads of width 64, causal) over log-normal documents (median 128,
+    sigma 1.5, 8 to 18,705 tokens) packed to 64k tokens: long sequences,
+    short ones and 16 causal packed windows in one call."""
+    import paper_2608_07524_amd as P
+    rng = np.random.default_rng(3)
+    pool = I.text_lengths(rng, 4096, median=128, sigma=1.5, lo=8).tolist()
+    lengths = I.greedy_pack(pool, 65536)[0]
+    w = I.Workload("Transformer-1D causal pack H48 D64", lengths, 48, 64, True, 1.0 / 8.0)
+    units, n_tiles, _ = P.work_list(w.cu_seqlens, 48, 64, True, 1)
+    assert len(units) > n_tiles, "the pack should hold packed windows"
+    bits, out = _run(torch, w, rng)
+    srng = np.random.default_rng(106)
+    q, k, v, do = _check_rows(bits, out, w, srng, 256, "T-1D causal")
+    _check_keys(q, k, v, do, out, w, srng, 4096, 3, "T-1D causal")
+    _check_identities(q, v, do, out, w, "T-1D causal")
+
+
 def _check_single_tokens(bits, out, w, label):
     """A one-token sequence attends to itself only: P = 1, so O = V and
     dV = dO exactly, and dS = dP - Delta = 0, so dK (and dQ) vanish in exact
