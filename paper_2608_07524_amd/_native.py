@@ -163,9 +163,21 @@ class _Desc:
 
 
 def _host_cu(cu_seqlens):
+    """cu_seqlens as a host int32 array; raises on values int32 cannot hold
+    (the C ABI reads int32) or on non-integer input."""
     if hasattr(cu_seqlens, "detach"):
         cu_seqlens = cu_seqlens.detach().cpu().numpy()
-    return np.asarray(cu_seqlens, dtype=np.int32)
+    a = np.asarray(cu_seqlens)
+    if a.ndim != 1 or a.size < 2:
+        raise ValueError("cu_seqlens must be a 1-D sequence of at least two offsets")
+    if a.dtype.kind not in "iu":
+        if a.dtype.kind == "f" and np.all(np.floor(a) == a):
+            a = a.astype(np.int64)
+        else:
+            raise ValueError("cu_seqlens must hold integers")
+    if int(a.min()) < 0 or int(a.max()) > np.iinfo(np.int32).max:
+        raise ValueError("cu_seqlens values must lie in [0, 2^31 - 1]")
+    return np.ascontiguousarray(a, dtype=np.int32)
 
 
 def _stream_ptr(torch, device):
@@ -186,18 +198,47 @@ def bwd_workspace_size(cu_seqlens, total_tokens, n_heads, head_dim, scale=1.0, c
     return n.value
 
 
-def _check_qkv(torch, *ts):
-    for t in ts:
-        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() or t.dim() != 3:
-            raise ValueError("tensors must be contiguous bf16 CUDA tensors of shape [T, H, D]")
+def _check_attn(torch, q, others=(), lse=None, workspace=None):
+    """Checks, before any library call, everything the C ABI cannot see
+    behind its raw pointers: q is a contiguous bf16 [T, H, D] tensor; every
+    tensor in ``others`` (name, tensor) has q's shape, dtype and device and is
+    contiguous; ``lse`` is contiguous fp32 [H, T] on that device; the
+    workspace is contiguous on that device.  Shapes and dtypes are checked
+    before the device, so a mismatch is reported as such on any device.
+    Returns (T, H, D)."""
+    if not hasattr(q, "dim") or q.dim() != 3:
+        raise ValueError("q must be a tensor of shape [T, H, D]")
+    if q.dtype != torch.bfloat16 or not q.is_contiguous():
+        raise ValueError("q must be a contiguous bf16 tensor")
+    for name, t in others:
+        if tuple(t.shape) != tuple(q.shape):
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, q has {tuple(q.shape)}")
+        if t.dtype != torch.bfloat16 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous bf16 tensor")
+    T, H, D = (int(x) for x in q.shape)
+    if lse is not None:
+        if tuple(lse.shape) != (H, T) or lse.dtype != torch.float32 or not lse.is_contiguous():
+            raise ValueError(f"lse must be a contiguous float32 tensor of shape ({H}, {T})")
+    if workspace is not None and not workspace.is_contiguous():
+        raise ValueError("workspace must be contiguous")
+    if not q.is_cuda:
+        raise ValueError("tensors must be on a CUDA (HIP) device")
+    for name, t in list(others) + [("lse", lse), ("workspace", workspace)]:
+        if t is not None and t.device != q.device:
+            raise ValueError(f"{name} is on {t.device}, q on {q.device}")
+    return T, H, D
+
+
+def _nbytes(t) -> int:
+    return int(t.numel()) * int(t.element_size())
 
 
 def varlen_attn_fwd(q, k, v, cu_seqlens, scale: Optional[float] = None, causal: bool = False,
                     out=None, lse=None, workspace=None):
     """O, LSE = attention over packed sequences (see dcp_varlen_attn_fwd)."""
     import torch
-    _check_qkv(torch, q, k, v)
-    T, H, D = q.shape
+    given = [("k", k), ("v", v)] + ([("out", out)] if out is not None else [])
+    T, H, D = _check_attn(torch, q, given, lse, workspace)
     scale = 1.0 / math.sqrt(D) if scale is None else scale
     d = _Desc(_host_cu(cu_seqlens), T, H, D, scale, causal)
     lib = load()
@@ -207,7 +248,7 @@ def varlen_attn_fwd(q, k, v, cu_seqlens, scale: Optional[float] = None, causal: 
     lse = torch.empty((H, T), dtype=torch.float32, device=q.device) if lse is None else lse
     ws = torch.empty(n.value, dtype=torch.uint8, device=q.device) if workspace is None else workspace
     _check(lib.dcp_varlen_attn_fwd(d.ref, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
-                                   ws.data_ptr(), ws.numel(), _stream_ptr(torch, q.device)))
+                                   ws.data_ptr(), _nbytes(ws), _stream_ptr(torch, q.device)))
     return o, lse
 
 
@@ -215,8 +256,9 @@ def varlen_attn_bwd(dout, o, lse, q, k, v, cu_seqlens, scale: Optional[float] = 
                     dq=None, dk=None, dv=None, workspace=None):
     """dQ, dK, dV of the loss <dO, O> (see dcp_varlen_attn_bwd)."""
     import torch
-    _check_qkv(torch, dout, o, q, k, v)
-    T, H, D = q.shape
+    given = [("k", k), ("v", v), ("dout", dout), ("o", o)]
+    given += [(n_, t) for n_, t in (("dq", dq), ("dk", dk), ("dv", dv)) if t is not None]
+    T, H, D = _check_attn(torch, q, given, lse, workspace)
     scale = 1.0 / math.sqrt(D) if scale is None else scale
     d = _Desc(_host_cu(cu_seqlens), T, H, D, scale, causal)
     lib = load()
@@ -228,7 +270,7 @@ def varlen_attn_bwd(dout, o, lse, q, k, v, cu_seqlens, scale: Optional[float] = 
     ws = torch.empty(n.value, dtype=torch.uint8, device=q.device) if workspace is None else workspace
     _check(lib.dcp_varlen_attn_bwd(d.ref, dout.data_ptr(), o.data_ptr(), lse.data_ptr(), q.data_ptr(),
                                    k.data_ptr(), v.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
-                                   ws.data_ptr(), ws.numel(), _stream_ptr(torch, q.device)))
+                                   ws.data_ptr(), _nbytes(ws), _stream_ptr(torch, q.device)))
     return dq, dk, dv
 
 
@@ -241,9 +283,8 @@ class PreparedAttention:
 
     def __init__(self, q, k, v, dout, cu_seqlens, scale: Optional[float] = None, causal: bool = False):
         import torch
-        _check_qkv(torch, q, k, v, dout)
+        T, H, D = _check_attn(torch, q, [("k", k), ("v", v), ("dout", dout)])
         self.torch = torch
-        T, H, D = q.shape
         self.scale = 1.0 / math.sqrt(D) if scale is None else scale
         self.d = _Desc(_host_cu(cu_seqlens), T, H, D, self.scale, causal)
         lib = self.lib = load()
@@ -288,7 +329,7 @@ def work_list(cu_seqlens, n_heads: int, head_dim: int, causal: bool, pass_: int)
     dcp_work_list): (units int32 [n, 5] = row0, seq0, seqlen, rows, head;
     n_tiles, the count of sequence-tile units before the packed windows;
     window_starts uint64 [n_windows, 4])."""
-    cu = np.asarray(cu_seqlens, dtype=np.int32)
+    cu = _host_cu(cu_seqlens)
     d = _Desc(cu, int(cu[-1]), n_heads, head_dim, 1.0, causal)
     lib = load()
     n, nt, nw = C.c_size_t(), C.c_size_t(), C.c_size_t()
@@ -482,7 +523,7 @@ class Layer:
             self.stash = None
         _check(self.lib.dcp_layer_fwd(C.byref(self.desc), C.byref(self.w), x.data_ptr(), out.data_ptr(),
                                       None if self.stash is None else self.stash.data_ptr(), self.ws.data_ptr(),
-                                      self.ws.numel(), self.stream))
+                                      _nbytes(self.ws), self.stream))
         return out
 
     def bwd(self, x, dout, dx=None):
@@ -491,6 +532,6 @@ class Layer:
         _check(self.lib.dcp_layer_bwd(C.byref(self.desc), C.byref(self.w), x.data_ptr(), dout.data_ptr(),
                                       dx.data_ptr(), C.byref(self.g),
                                       None if self.stash is None else self.stash.data_ptr(), self.ws.data_ptr(),
-                                      self.ws.numel(), self.stream))
+                                      _nbytes(self.ws), self.stream))
         self.stash = None
         return dx

@@ -130,3 +130,51 @@ def test_layer_validation():
     assert lib.dcp_layer_fwd(C.byref(L), C.byref(w), fake, fake, None, fake, f.value - 1, None) == N.DCP_ERR_WORKSPACE
     assert lib.dcp_layer_bwd(C.byref(L), C.byref(w), fake, fake, fake, C.byref(w), None, fake, b.value - 1, None) \
         == N.DCP_ERR_WORKSPACE
+
+
+# ---------------------------------------------------------------------------
+# the Python binding checks what the C ABI cannot see behind raw pointers
+
+def _bf(*shape):
+    import torch
+    return torch.zeros(shape, dtype=torch.bfloat16)
+
+
+def test_binding_rejects_mismatched_tensors_before_any_call():
+    import torch
+    q = _bf(16, 2, 64)
+    cu = [0, 16]
+    cases = [
+        dict(k=_bf(8, 2, 64)),                         # shorter k: the kernels would read past it
+        dict(v=_bf(16, 2, 72)),
+        dict(k=torch.zeros(16, 2, 64, dtype=torch.float16)),
+        dict(v=_bf(16, 64, 2).transpose(1, 2)),        # non-contiguous
+        dict(out=_bf(16, 1, 64)),
+        dict(lse=torch.zeros(16, 2, dtype=torch.float32)),   # [T, H] instead of [H, T]
+        dict(lse=torch.zeros(2, 16, dtype=torch.bfloat16)),
+    ]
+    for kw in cases:
+        args = dict(k=_bf(16, 2, 64), v=_bf(16, 2, 64))
+        args.update(kw)
+        with pytest.raises(ValueError) as e:
+            P.varlen_attn_fwd(q, args.pop("k"), args.pop("v"), cu, 0.125, **args)
+        assert "device" not in str(e.value), kw
+    bwd_cases = [dict(dout=_bf(16, 2, 32)), dict(o=_bf(15, 2, 64)), dict(dq=_bf(16, 2, 64)[:, :1]),
+                 dict(dk=_bf(17, 2, 64)), dict(lse=torch.zeros(2, 15, dtype=torch.float32))]
+    for kw in bwd_cases:
+        args = dict(dout=_bf(16, 2, 64), o=_bf(16, 2, 64), lse=torch.zeros(2, 16, dtype=torch.float32))
+        args.update(kw)
+        with pytest.raises(ValueError) as e:
+            P.varlen_attn_bwd(args.pop("dout"), args.pop("o"), args.pop("lse"), q, _bf(16, 2, 64), _bf(16, 2, 64),
+                              cu, 0.125, **args)
+        assert "device" not in str(e.value), kw
+    # well-formed host tensors are refused for their device, still before any call
+    with pytest.raises(ValueError, match="device"):
+        P.varlen_attn_fwd(q, _bf(16, 2, 64), _bf(16, 2, 64), cu, 0.125)
+
+
+@pytest.mark.parametrize("cu", [[0, 1 << 31], [0, -1, 4], [0.5, 4], [[0, 4]]])
+def test_binding_rejects_cu_seqlens_outside_int32(cu):
+    from paper_2608_07524_amd._native import _host_cu
+    with pytest.raises(ValueError):
+        _host_cu(cu)

@@ -62,6 +62,63 @@ def test_hand_example_accumulation():
     assert P.accumulation_steps([3, 5, 4], 6, 4) == ([8, 4, 6], 4, 24)
 
 
+# ------------------------------------------------ communication hand example
+# The Ulysses all-to-all term of a candidate (p > 1): four all-to-alls per
+# layer in the forward (Q, K, V to head shards, O back) and four in the
+# backward (dO out; dQ, dK, dV back).  Each device holds b*S/p tokens of
+# `hidden` bf16 values and sends a 1/p share of them to each peer, so every
+# link of a fully connected node carries 2*b*S*hidden/p^2 bytes:
+#     c(b, p) = 4 * (alpha + ceil(2*b*S*hidden / (p^2 * beta)))      (p > 1)
+# Inputs: one row s = 1000 with t_f = 400000, t_b = 800000, m = 0,
+# m_inp = 1000 per layer; L = 2, T_C = 0, M_C = 0, budget 1500;
+# hidden = 96, alpha = 100 ns, beta = 7 bytes/ns, p in {1, 2, 4}, 4 heads.
+# Memory (Eq. (6), r = L): M = 2*ceil(b*1000/p) -> p = 1 needs 2000 > 1500
+# (infeasible), (p=2, b=1) 1000, (p=4, b=1) 500, (p=4, b=2) 1000,
+# (p=2, b=2) 2000 (infeasible).  m = 0, so no layer is recomputed (r = 0).
+# Per-link volume 2*b*1000*96 = 192000*b bytes:
+#   (p=2, b=1): 192000/28  = 6857.14 -> 6858, c = 4*(100+6858) = 27832
+#               t_f = 200000+27832 = 227832, t_b = 400000+27832 = 427832
+#               T = 2*(t_f+t_b) = 1311328, p*T/b = 2622656
+#   (p=4, b=1): 192000/112 = 1714.29 -> 1715, c = 4*1815 = 7260
+#               t_f = 107260, t_b = 207260, T = 629040, p*T/b = 2516160
+#   (p=4, b=2): 384000/112 = 3428.57 -> 3429, c = 4*3529 = 14116
+#               t_f = 200000+14116 = 214116, t_b = 414116, T = 1256464,
+#               p*T/b = 2512928
+# Eq. (1) throughput b/(p*T): with b_max = 1, (p=4, b=1, T=629040) beats
+# (p=2, T=1311328); with b_max = 2, (p=4, b=2, T=1256464) wins because the
+# latency alpha is paid once for twice the tokens.  Mistakes this catches:
+# p instead of p^2 gives c = 55260 at p = 2 and 27832 at p = 4, and then
+# (p=2) wins (2842080 < 2845312); eight all-to-alls instead of four double
+# every c; a floor instead of the ceiling gives 27828 and 7256.
+# A pack of 300 + 500 tokens (both take the s = 500 row, t_f = 200000,
+# t_b = 400000, m_inp = 500 each) moves S = 800 tokens, not the rows' 1000:
+#   (p=2): 153600/28 = 5485.71 -> 5486, c = 22344, T = 2*(222344+422344) = 1289376
+#   (p=4): 153600/112 = 1371.43 -> 1372, c = 5888, T = 2*(105888+205888) = 623552
+
+COMM_OPTS = dict(sp_cands=(1, 2, 4), n_heads=4, hidden=96, a2a_alpha_ns=100, link_bytes_per_ns=7, g_min=1, g_max=4)
+COMM_TABLE = ((500, 200000, 400000, 0, 500), (1000, 400000, 800000, 0, 1000))
+
+
+def test_comm_hand_example():
+    t = _table(COMM_TABLE, L=2, T_C=0, M_C=0)
+    for mode in (P.MODE_INTRA, P.MODE_INTER):
+        out = P.plan([1000], t, 1500, P.PlanOpts(b_max=1, mode=mode, **COMM_OPTS))
+        r = 0 if mode == P.MODE_INTRA else 2
+        # (full recomputation adds r*t_f: 2*107260)
+        assert (out.sp_size, out.micro_batch, out.recompute_layers) == ([4], [1], [r])
+        assert out.step_time_ns == [629040 + r * 107260] and out.mem_bytes == [500]
+    out = P.plan([1000], t, 1500, P.PlanOpts(b_max=2, **COMM_OPTS))
+    assert (out.sp_size, out.micro_batch, out.step_time_ns, out.mem_bytes) == ([4], [2], [1256464], [1000])
+    # each p alone: the step times of the derivation above
+    assert P.plan([1000], t, 1500, P.PlanOpts(b_max=1, **dict(COMM_OPTS, sp_cands=(2,)))).step_time_ns == [1311328]
+    assert P.plan([1000], t, 1500, P.PlanOpts(b_max=1, **dict(COMM_OPTS, sp_cands=(4,)))).step_time_ns == [629040]
+    # a pack moves its own tokens
+    pk = P.plan([300, 500], t, 1500, P.PlanOpts(b_max=1, **dict(COMM_OPTS, sp_cands=(2,))), batch_offsets=[0, 2])
+    assert pk.step_time_ns == [1289376]
+    pk = P.plan([300, 500], t, 1500, P.PlanOpts(b_max=1, **COMM_OPTS), batch_offsets=[0, 2])
+    assert (pk.sp_size, pk.step_time_ns) == ([4], [623552])
+
+
 # ------------------------------------------------------------ brute force pins
 
 def _random_case(rng):

@@ -54,6 +54,23 @@ def test_hand_example():
                                        link_bytes_per_ns=1, mode=mode))
 
 
+def test_comm_hand_example():
+    """The C++ planner on the communication example whose step times are
+    worked out by hand in tests/test_oracle_planner.py (Ulysses all-to-all
+    term, p in {2, 4}, alpha > 0, hidden > 0)."""
+    rows = [(500, 200000, 400000, 0, 500), (1000, 400000, 800000, 0, 1000)]
+    kw = dict(sp_cands=(1, 2, 4), n_heads=4, hidden=96, a2a_alpha_ns=100, link_bytes_per_ns=7, g_min=1, g_max=4)
+    out = P.plan([1000], rows, 2, 0, 0, 1500, b_max=1, **kw)
+    assert (out.sp_size, out.micro_batch, out.recompute_layers, out.step_time_ns) == ([4], [1], [0], [629040])
+    out = P.plan([1000], rows, 2, 0, 0, 1500, b_max=1, mode=0, **kw)
+    assert (out.recompute_layers, out.step_time_ns) == ([2], [629040 + 2 * 107260])
+    out = P.plan([1000], rows, 2, 0, 0, 1500, b_max=2, **kw)
+    assert (out.sp_size, out.micro_batch, out.step_time_ns, out.mem_bytes) == ([4], [2], [1256464], [1000])
+    assert P.plan([1000], rows, 2, 0, 0, 1500, b_max=1, **dict(kw, sp_cands=(2,))).step_time_ns == [1311328]
+    out = P.plan([300, 500], rows, 2, 0, 0, 1500, batch_offsets=[0, 2], b_max=1, **kw)
+    assert (out.sp_size, out.step_time_ns) == ([4], [623552])
+
+
 def _ci_table(L=28, h=256):
     # per-layer attention-like costs of the tiny packed configuration
     rows = []
