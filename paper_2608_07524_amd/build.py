@@ -36,8 +36,8 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found; ROCm is required to build libdcp")
 
 
-def _compile(hipcc: str, src: str, obj: str, extra):
-    cmd = [hipcc, *COMMON_FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(hipcc: str, src: str, obj: str):
+    cmd = [hipcc, *COMMON_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".hip"):
         cmd[1:1] = ["-x", "hip"]
         cmd += DEVICE_FLAGS
@@ -48,14 +48,13 @@ def _compile(hipcc: str, src: str, obj: str, extra):
     return err
 
 
-def build(verbose: bool = False, extra=(), out: str = LIB, build_dir: str = BUILD_DIR) -> str:
-    """Compile and link; ``extra`` flags go to every compile (e.g. tile-shape
-    -D overrides), ``out`` is the library path."""
+def build(verbose: bool = False, out: str = LIB, build_dir: str = BUILD_DIR) -> str:
+    """Compile every source and link ``out`` (the in-tree libdcp.so by default)."""
     hipcc = _hipcc()
     os.makedirs(build_dir, exist_ok=True)
     objs = [os.path.join(build_dir, os.path.splitext(s)[0] + ".o") for s in SOURCES]
     with ThreadPoolExecutor(max_workers=min(6, len(SOURCES))) as ex:
-        logs = list(ex.map(lambda so: _compile(hipcc, so[0], so[1], list(extra)), zip(SOURCES, objs)))
+        logs = list(ex.map(lambda so: _compile(hipcc, so[0], so[1]), zip(SOURCES, objs)))
     if verbose:
         for s, log in zip(SOURCES, logs):
             if log.strip():

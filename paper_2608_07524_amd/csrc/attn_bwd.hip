@@ -38,10 +38,6 @@
 namespace dcp {
 namespace {
 
-#ifndef DCP_BWD_OSTR
-#define DCP_BWD_OSTR 1  // 0: one-copy tiles at the minimal row-read stride
-#endif
-
 template <int D>
 struct BwdShape {
   static constexpr int DP = (D + 15) / 16 * 16;  // contraction width (zero padded)
@@ -68,7 +64,7 @@ struct BwdShape {
   // banks (only the two row groups 16 apart, always on the same banks,
   // meet); at D = 128, 152 elements leaves two-way overlaps where the
   // minimal 136 stacks four.
-  static constexpr int OSTR = !DCP_BWD_OSTR ? DP + 8 : D == 72 ? 104 : D == 128 ? 152 : DP + 8;
+  static constexpr int OSTR = D == 72 ? 104 : D == 128 ? 152 : DP + 8;
   static_assert(OSTR % 16 == 8 && OSTR >= (KV16 ? NMB * 16 : NDB * 32), "one-copy stride");
 };
 

@@ -92,15 +92,8 @@ __device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const 
 // Wavefront issue priority around matrix-core phases: with two wavefronts
 // on a SIMD, the one feeding the matrix cores issues first and the other
 // fills the gaps with vector work.
-#ifndef DCP_MFMA_PRIO
-#define DCP_MFMA_PRIO 1
-#endif
-__device__ __forceinline__ void mfma_prio_hi() {
-  if (DCP_MFMA_PRIO) __builtin_amdgcn_s_setprio(1);
-}
-__device__ __forceinline__ void mfma_prio_lo() {
-  if (DCP_MFMA_PRIO) __builtin_amdgcn_s_setprio(0);
-}
+__device__ __forceinline__ void mfma_prio_hi() { __builtin_amdgcn_s_setprio(1); }
+__device__ __forceinline__ void mfma_prio_lo() { __builtin_amdgcn_s_setprio(0); }
 
 // Max / sum of a value with the lane 32 positions away (the two halves of a
 // wavefront), via the gfx950 cross-half lane swap.

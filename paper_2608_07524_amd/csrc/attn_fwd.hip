@@ -35,21 +35,11 @@ namespace dcp {
 namespace {
 
 constexpr int kFwdBN = 64;
-#ifndef DCP_FWD_STAGES
-#define DCP_FWD_STAGES 4
-#endif
-#ifndef DCP_FWD_SCHED
-#define DCP_FWD_SCHED 0
-#endif
 // Ring depth: tile kt + kFwdStages - 1 streams in while tile kt is consumed.
-constexpr int kFwdStages = DCP_FWD_STAGES;
+constexpr int kFwdStages = 4;
 static_assert(kFwdStages >= 3 && kWinFwdStages >= 3, "tiles kt and kt + 1 are read while kt + 2 lands");
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 constexpr float kNoMax = -1e30f;       // running max before any key
-
-#ifndef DCP_FWD_VSKEW
-#define DCP_FWD_VSKEW 1
-#endif
 
 template <int D>
 struct FwdShape {
@@ -74,23 +64,11 @@ struct FwdShape {
   // same banks (16 rows x 64 mod 128 bytes = 0 mod 256); starting every
   // 16-row group of the V tile 32 bytes further on moves the second set of
   // rows onto the other half of each bank run.
-  static constexpr int VSKEW = (PV16 && DCP_FWD_VSKEW) ? 16 : 0;
+  static constexpr int VSKEW = PV16 ? 16 : 0;
 };
 
-// Interleaving hints for the compiler's scheduler (masks of
-// __builtin_amdgcn_sched_group_barrier).
-constexpr int kSchedMfma = 0x008;
-constexpr int kSchedValu = 0x002;
-constexpr int kSchedDsRead = 0x100;
-
-#ifdef DCP_FWD_WPE
-#define DCP_FWD_OCCUPANCY __attribute__((amdgpu_waves_per_eu(DCP_FWD_WPE)))
-#else
-#define DCP_FWD_OCCUPANCY
-#endif
-
 template <int D, int NW, bool CAUSAL, bool PACKED, int STAGES>
-__global__ __launch_bounds__(64 * NW) DCP_FWD_OCCUPANCY void attn_fwd_kernel(const __bf16* __restrict__ q,
+__global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restrict__ q,
                                                            const __bf16* __restrict__ k,
                                                            const __bf16* __restrict__ v, __bf16* __restrict__ o,
                                                            float* __restrict__ lse,
@@ -385,21 +363,6 @@ __global__ __launch_bounds__(64 * NW) DCP_FWD_OCCUPANCY void attn_fwd_kernel(con
     }
     if constexpr (MASK) apply_mask(sn, bn);
     pv_product(pb, vcur);
-    if (DCP_FWD_SCHED) {
-      // every LDS read first, then the S products of the next block between
-      // the exponentials, then the PV products between the row-max steps
-      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, NKD + 4 * NDB, 0);
-#pragma unroll
-      for (int i = 0; i < NKD; ++i) {
-        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(kSchedValu, 40 / NKD, 0);
-      }
-#pragma unroll
-      for (int i = 0; i < 2 * NDB; ++i) {
-        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(kSchedValu, 2, 0);
-      }
-    }
     rescale(row_max(sn), valid_next);
     sc = sn;
   };

@@ -7,10 +7,7 @@
 namespace dcp {
 
 // Query rows per forward workgroup: kFwdWaves wavefronts x 32.
-#ifndef DCP_FWD_WAVES
-#define DCP_FWD_WAVES 8
-#endif
-constexpr int kFwdWaves = DCP_FWD_WAVES;
+constexpr int kFwdWaves = 8;
 // Backward, dK/dV pass: `waves` wavefronts per workgroup, each owning
 // 32*kb keys whose K, V fragments and dK, dV accumulators stay resident,
 // stepping over `bm` queries at a time through a `stages`-deep LDS ring;
@@ -31,107 +28,38 @@ struct DkdvShape {
   int kb, waves, bm, stages, waves_per_eu;
   bool onecopy;  // the ring holds Q and dO once (row-read stride) instead of twice
 };
-#ifndef DCP_DKDV_KB
-#define DCP_DKDV_KB 1
-#endif
-#ifndef DCP_DKDV_WAVES
-#define DCP_DKDV_WAVES 8
-#endif
-#ifndef DCP_DKDV_BM
-#define DCP_DKDV_BM 64
-#endif
-#ifndef DCP_DKDV_WPE
-#define DCP_DKDV_WPE 2
-#endif
-#ifndef DCP_DKDV_STAGES
-#define DCP_DKDV_STAGES 4
-#endif
-#ifndef DCP_DKDV_ONECOPY
-#define DCP_DKDV_ONECOPY 1
-#endif
-#ifndef DCP_DKDV_KB_D128
-#define DCP_DKDV_KB_D128 1
-#endif
-#ifndef DCP_DKDV_WAVES_D128
-#define DCP_DKDV_WAVES_D128 4
-#endif
-#ifndef DCP_DKDV_BM_D128
-#define DCP_DKDV_BM_D128 128
-#endif
-#ifndef DCP_DKDV_STAGES_D128
-#define DCP_DKDV_STAGES_D128 2
-#endif
-#ifndef DCP_DKDV_ONECOPY_D128
-#define DCP_DKDV_ONECOPY_D128 1
-#endif
-#ifndef DCP_BWD_DQ_WAVES
-#define DCP_BWD_DQ_WAVES 8
-#endif
 constexpr DkdvShape bwd_dkdv_shape(int head_dim) {
-  return head_dim > 96 ? DkdvShape{DCP_DKDV_KB_D128, DCP_DKDV_WAVES_D128, DCP_DKDV_BM_D128, DCP_DKDV_STAGES_D128, 1,
-                                   DCP_DKDV_ONECOPY_D128 != 0}
-                       : DkdvShape{DCP_DKDV_KB, DCP_DKDV_WAVES, DCP_DKDV_BM, DCP_DKDV_STAGES, DCP_DKDV_WPE,
-                                   DCP_DKDV_ONECOPY != 0};
+  return head_dim > 96 ? DkdvShape{1, 4, 128, 2, 1, true} : DkdvShape{1, 8, 64, 4, 2, true};
 }
-constexpr int kBwdDqWaves = DCP_BWD_DQ_WAVES;
+constexpr int kBwdDqWaves = 8;
 constexpr int kBwdDqBN = 64;
-#ifndef DCP_BWD_DQ_STAGES
-#define DCP_BWD_DQ_STAGES 3
-#endif
-#ifndef DCP_BWD_DQ_STAGES_D128
-#define DCP_BWD_DQ_STAGES_D128 2
-#endif
-#ifndef DCP_BWD_DQ_ONECOPY
-#define DCP_BWD_DQ_ONECOPY 1
-#endif
-constexpr int kBwdDqStages = DCP_BWD_DQ_STAGES;
-constexpr int kBwdDqStagesD128 = DCP_BWD_DQ_STAGES_D128;
-constexpr bool kBwdDqOneCopy = DCP_BWD_DQ_ONECOPY != 0;
+constexpr int kBwdDqStages = 3;
+constexpr int kBwdDqStagesD128 = 2;
+constexpr bool kBwdDqOneCopy = true;
 
 // Packed windows (runs of short sequences sharing one tile) launch with
 // their own shape: fewer wavefronts per workgroup (smaller tiles) and a
 // shallower ring -- for the dK/dV pass also 32-query ring tiles -- so that
 // two workgroups share a CU; a window then spans at most that many rows.
-#ifndef DCP_WIN_FWD_WAVES
-#define DCP_WIN_FWD_WAVES 4
-#endif
-#ifndef DCP_WIN_FWD_STAGES
-#define DCP_WIN_FWD_STAGES 3
-#endif
-#ifndef DCP_WIN_DQ_WAVES
-#define DCP_WIN_DQ_WAVES 4
-#endif
-#ifndef DCP_WIN_DQ_STAGES
-#define DCP_WIN_DQ_STAGES 2
-#endif
-#ifndef DCP_WIN_DKDV_WAVES
-#define DCP_WIN_DKDV_WAVES 4
-#endif
-#ifndef DCP_WIN_DKDV_STAGES
-#define DCP_WIN_DKDV_STAGES 3
-#endif
-#ifndef DCP_WIN_DKDV_BM
-#define DCP_WIN_DKDV_BM 32
-#endif
-constexpr int kWinFwdWaves = DCP_WIN_FWD_WAVES;
-constexpr int kWinFwdStages = DCP_WIN_FWD_STAGES;
-constexpr int kWinDqWaves = DCP_WIN_DQ_WAVES;
-constexpr int kWinDqStages = DCP_WIN_DQ_STAGES;
+constexpr int kWinFwdWaves = 4;
+constexpr int kWinFwdStages = 3;
+constexpr int kWinDqWaves = 4;
+constexpr int kWinDqStages = 2;
+constexpr int kWinDkdvWaves = 4;
+constexpr int kWinDkdvStages = 3;
+constexpr int kWinDkdvBM = 32;
 constexpr DkdvShape bwd_dkdv_window_shape(int head_dim) {
   return head_dim > 96 ? bwd_dkdv_shape(head_dim)
-                       : DkdvShape{1, DCP_WIN_DKDV_WAVES, DCP_WIN_DKDV_BM, DCP_WIN_DKDV_STAGES, DCP_DKDV_WPE, false};
+                       : DkdvShape{1, kWinDkdvWaves, kWinDkdvBM, kWinDkdvStages, bwd_dkdv_shape(head_dim).waves_per_eu,
+                                   false};
 }
 // Every query and key of a packed window lies inside the window, so at head
 // widths up to 96 one workgroup computes dQ of its window as well as dK and
 // dV (dS goes through LDS instead of being recomputed by the dQ pass), and
 // the dQ pass skips the windows.  This needs the two passes to cut the same
 // windows (equal window sizes).
-#ifndef DCP_WIN_FUSED
-#define DCP_WIN_FUSED 1
-#endif
 constexpr bool bwd_window_fused(int head_dim) {
-  return DCP_WIN_FUSED && head_dim <= 96 && DCP_WIN_DKDV_BM == 32 &&
-         32 * DCP_WIN_DKDV_WAVES == 32 * DCP_WIN_DQ_WAVES;
+  return head_dim <= 96 && kWinDkdvBM == 32 && kWinDkdvWaves == kWinDqWaves;
 }
 
 struct FwdArgs {
