@@ -127,6 +127,50 @@ int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, const void*
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Prepared batches.  A training step runs the forward and the backward of
+ * the same packed batch, and a profiler or benchmark runs them many times:
+ * the tile lists of the three kernel passes (forward, dK/dV, dQ) depend only
+ * on cu_seqlens, so they are built once on the host (dcp_batch_create) and
+ * copied once into a caller-owned device buffer (dcp_batch_upload); every
+ * later dcp_batch_fwd / dcp_batch_bwd on that buffer only launches kernels
+ * (no host list building, no host-to-device copy).  Results equal those of
+ * dcp_varlen_attn_fwd / _bwd bit for bit (same kernels, same lists).
+ *
+ *   dcp_batch_create   host only: validates `desc` (as the calls above do),
+ *                      copies it and its cu_seqlens, builds the three lists.
+ *                      *out is an opaque host handle (NULL on failure).
+ *   dcp_batch_workspace_size  bytes of the device buffer: the constant
+ *                      chunks, the three lists with their window masks, and
+ *                      the backward's fp32 scratch (LSE*log2e and -Delta,
+ *                      [H, T] each).
+ *   dcp_batch_upload   enqueues the copy of the lists into `workspace`
+ *                      (device, 256-byte aligned, at least the size above)
+ *                      on `stream` and remembers that buffer and the current
+ *                      device; uploading again (to the same or another
+ *                      buffer) is allowed.
+ *   dcp_batch_fwd/bwd  as dcp_varlen_attn_fwd / _bwd for the batch's
+ *                      descriptor; `workspace` must be the buffer of the last
+ *                      upload, on the device current at that upload
+ *                      (DCP_ERR_INVALID otherwise), and calls are ordered
+ *                      after the upload by the stream (or by the caller's
+ *                      synchronisation when streams differ).  Calls that
+ *                      share one buffer must not overlap in time: the
+ *                      backward writes its scratch there.
+ *   dcp_batch_destroy  frees the handle (host memory only; NULL is a no-op).
+ *                      The device buffer stays the caller's.
+ */
+typedef struct dcp_batch_s* dcp_batch;
+int dcp_batch_create(const dcp_attn_desc* desc, dcp_batch* out);
+int dcp_batch_workspace_size(dcp_batch batch, size_t* bytes);
+int dcp_batch_upload(dcp_batch batch, void* workspace, size_t workspace_bytes, void* stream);
+int dcp_batch_fwd(dcp_batch batch, const void* q, const void* k, const void* v, void* o, float* lse,
+                  void* workspace, size_t workspace_bytes, void* stream);
+int dcp_batch_bwd(dcp_batch batch, const void* dout, const void* o, const float* lse, const void* q,
+                  const void* k, const void* v, void* dq, void* dk, void* dv, void* workspace,
+                  size_t workspace_bytes, void* stream);
+void dcp_batch_destroy(dcp_batch batch);
+
+/*
  * The work the attention kernels run for `desc` (introspection for
  * schedulers and tests: launches nothing, needs no GPU).  pass 0 is the
  * forward, 1 the dK/dV pass, 2 the dQ pass (at head widths up to 96 the dQ
@@ -205,7 +249,11 @@ int dcp_profile_workspace_size(int64_t max_len, const dcp_profile_opts* opts, si
 /*
  * Measure one row per length: a single sequence of lengths[i] tokens with
  * the given heads and width, synthetic inputs written into the workspace,
- * forward and backward timed with HIP events on `stream`.  Synchronises.
+ * forward and backward timed with HIP events on `stream`.  Each length's
+ * work lists are built and uploaded before its first run; the warm-up and
+ * timed runs are then enqueued back to back with events around every timed
+ * forward and backward, so the rows hold device time, not host time.
+ * Synchronises.
  *   lengths   host int64 [n], each in [1, max_len used for the workspace].
  *   out_rows  host [n], written only on success.
  */

@@ -20,7 +20,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdcp.so")
 
-SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "layer.hip", "dcp_api.cpp", "dcp_plan.cpp", "layer_api.cpp"]
+SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "layer.hip", "dcp_api.cpp", "dcp_error.cpp", "work_list.cpp", "dcp_plan.cpp",
+           "layer_api.cpp"]
 
 # Packed fp32 vector ops stay disabled for device code (plain scalar fp32
 # VALU only); the host pass reports the feature as unknown, which is benign.

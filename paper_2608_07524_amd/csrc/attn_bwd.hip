@@ -1025,17 +1025,6 @@ __global__ void fill_bf16_kernel(__bf16* p, int64_t n, uint32_t seed) {
 
 }  // namespace
 
-int bwd_key_tile_rows(int head_dim) {
-  const DkdvShape sh = bwd_dkdv_shape(head_dim);
-  return 32 * sh.kb * sh.waves;
-}
-int bwd_query_tile_rows(int head_dim) { return 32 * kBwdDqWaves; }
-int bwd_key_window_rows(int head_dim) {
-  const DkdvShape sh = bwd_dkdv_window_shape(head_dim);
-  return 32 * sh.kb * sh.waves;
-}
-int bwd_query_window_rows(int head_dim) { return 32 * kWinDqWaves; }
-
 hipError_t launch_bwd(const BwdArgs& a) {
   switch (a.head_dim) {
     case 64: return a.causal ? launch_bwd_t<64, true>(a) : launch_bwd_t<64, false>(a);

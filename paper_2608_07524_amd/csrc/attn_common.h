@@ -14,6 +14,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "tile_shapes.h"
+
 namespace dcp {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -24,24 +26,6 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-// One tile of work: rows [row0, row0 + rows) of the packed tensor for head
-// `head`, all in the sequence that occupies rows [seq0, seq0 + seqlen).
-// rows == 0 marks padding (the workgroup exits at once).
-// A negative seqlen marks a packed window instead: consecutive sequences,
-// each shorter than a tile, sharing one tile of `rows` rows that starts at
-// row0 == seq0.  Row i of the window attends only to rows of its own
-// sequence; -seqlen - 1 indexes the window's mask of sequence starts (four
-// 64-bit words, bit x set where a sequence starts at window offset x).
-struct WorkUnit {
-  int32_t row0;
-  int32_t seq0;
-  int32_t seqlen;
-  uint16_t rows;  // at most one tile (256)
-  uint16_t head;  // head counts are limited to 65535 by the C ABI
-};
-static_assert(sizeof(WorkUnit) == 16, "16 bytes per tile");
-constexpr int kWindowWords = 4;  // 64-bit words per window mask: windows hold at most 256 rows
 
 // Bounds [lo, hi) of the sequence holding window offset x (0 <= x < n,
 // the window's length), from the window's mask of sequence starts (bit 0
@@ -65,7 +49,6 @@ __device__ __forceinline__ void window_bounds(const uint64_t* __restrict__ start
 // (scratch memory) and spill the caller's live registers around it.
 #define DCP_INLINE __attribute__((always_inline))
 
-constexpr int kNumXcd = 8;  // MI355X: 8 accelerator dies, each with its own L2
 
 // The dispatcher hands workgroup i to die i % 8.  Work lists are laid out
 // as 8 consecutive per-die lists of `per_xcd` entries, so a die walks its
@@ -330,11 +313,5 @@ struct DmaVecPair {
   }
 };
 
-// Offsets (bf16 elements) of the 16-byte constant chunks every attention
-// workspace starts with.
-constexpr int kConstZero = 0;   // [0, 0, 0, 0, 0, 0, 0, 0]
-constexpr int kConstOnes = 8;   // [1, 0, 0, 0, 0, 0, 0, 0]
-constexpr int kConstInf = 16;   // fp32 +inf (a query past its sequence end)
-constexpr int kConstBytes = 256;
 
 }  // namespace dcp

@@ -474,9 +474,6 @@ hipError_t launch_fwd_t(const FwdArgs& a) {
 
 }  // namespace
 
-int fwd_tile_rows(int head_dim) { return kFwdWaves * 32; }
-int fwd_window_rows(int head_dim) { return kWinFwdWaves * 32; }
-
 hipError_t launch_fwd(const FwdArgs& a) {
   if (a.n_units == 0 && a.n_wunits == 0) return hipSuccess;
   constexpr int W = kFwdWaves;

@@ -1,39 +1,21 @@
-// C ABI of libdcp: argument validation, work lists, workspace layout,
-// kernel launches and the per-length cost profiler.
+// C ABI of libdcp: device checks, work-list uploads, kernel launches, the
+// prepared-batch handle and the per-length cost profiler.  Argument
+// validation and the work lists themselves are host code (work_list.cpp).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cmath>
-#include <cstdio>
 #include <cstring>
-#include <initializer_list>
-#include <limits>
 #include <mutex>
-#include <string>
-#include <utility>
+#include <new>
 #include <vector>
 
 #include "attn_common.h"
 #include "attn_launch.h"
 #include "dcp_internal.h"
+#include "work_list.h"
 
 namespace dcp {
-
-namespace {
-thread_local std::string g_last_error;
-}
-
-int fail(int code, const char* fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
-  va_end(ap);
-  g_last_error = buf;
-  return code;
-}
-
-void clear_error() { g_last_error.clear(); }
 
 KernelEvents& kernel_events() {
   thread_local KernelEvents ev;
@@ -42,14 +24,12 @@ KernelEvents& kernel_events() {
 
 namespace {
 
-constexpr size_t kAlign = 256;
-inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
-
 // The kernels are built for gfx950 only; refuse other devices up front.
-int check_device() {
+int check_device(int* device = nullptr) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "no HIP device: %s", hipGetErrorString(e));
+  if (device) *device = dev;
   static std::mutex mu;
   static std::vector<int> ok_devices;
   {
@@ -66,205 +46,6 @@ int check_device() {
   return DCP_OK;
 }
 
-int validate_desc(const dcp_attn_desc* d) {
-  if (!d) return fail(DCP_ERR_INVALID, "desc is null");
-  if (d->n_seqs < 1) return fail(DCP_ERR_INVALID, "n_seqs must be >= 1");
-  if (!d->cu_seqlens_host) return fail(DCP_ERR_INVALID, "cu_seqlens_host is null");
-  if (d->total_tokens < 0 || d->total_tokens >= (int64_t(1) << 31))
-    return fail(DCP_ERR_INVALID, "total_tokens must be in [0, 2^31)");
-  if (d->n_heads < 1 || d->n_heads > 65535) return fail(DCP_ERR_INVALID, "n_heads must be in [1, 65535]");
-  if (d->head_dim != 64 && d->head_dim != 72 && d->head_dim != 128)
-    return fail(DCP_ERR_UNSUPPORTED, "head_dim %d is not supported (64, 72, 128)", d->head_dim);
-  if (!(std::isfinite(d->scale) && d->scale > 0.f)) return fail(DCP_ERR_INVALID, "scale must be finite and > 0");
-  if (d->causal != 0 && d->causal != 1) return fail(DCP_ERR_INVALID, "causal must be 0 or 1");
-  const int32_t* cu = d->cu_seqlens_host;
-  if (cu[0] != 0) return fail(DCP_ERR_INVALID, "cu_seqlens[0] must be 0");
-  for (int32_t b = 0; b < d->n_seqs; ++b)
-    if (cu[b + 1] < cu[b]) return fail(DCP_ERR_INVALID, "cu_seqlens must be non-decreasing (index %d)", b + 1);
-  if (cu[d->n_seqs] > d->total_tokens)
-    return fail(DCP_ERR_INVALID, "cu_seqlens[n] = %d exceeds total_tokens", cu[d->n_seqs]);
-  const int64_t elems = d->total_tokens * int64_t(d->n_heads) * d->head_dim;
-  if (elems / d->n_heads / d->head_dim != d->total_tokens) return fail(DCP_ERR_INVALID, "tensor size overflows");
-  return DCP_OK;
-}
-
-int check_tensor(const void* p, const char* name) {
-  if (!p) return fail(DCP_ERR_INVALID, "%s is null", name);
-  if (reinterpret_cast<uintptr_t>(p) % 16 != 0) return fail(DCP_ERR_INVALID, "%s must be 16-byte aligned", name);
-  return DCP_OK;
-}
-
-// Tiles of `tile` rows per (sequence, head), never straddling two
-// sequences, laid out as 8 per-die lists (see unit_for_block).  Runs of
-// consecutive sequences shorter than `window_tile` (<= tile) share one
-// tile as a packed window of at most `window_tile` rows (each row still
-// attends only within its own sequence), so thousands of short sequences do
-// not each occupy a mostly idle workgroup.  Work of a tile: the keys it visits (forward, dQ
-// pass) or the queries visiting it (dK/dV pass); a window's is its row
-// count.  The (sequence, chunk) and window groups -- long sequences split
-// into chunks when a few of them would otherwise leave dies idle -- are
-// assigned to the least-loaded die, longest first; each die's list keeps a
-// chunk's tiles together (they share K/V or Q/dO in that die's L2) and is
-// padded with empty tiles to the longest list.
-size_t tiles_per_head(const dcp_attn_desc* d, int tile) {
-  size_t n = 0;
-  for (int32_t b = 0; b < d->n_seqs; ++b)
-    n += size_t((d->cu_seqlens_host[b + 1] - d->cu_seqlens_host[b] + tile - 1) / tile);
-  return n;
-}
-
-struct UnitList {
-  std::vector<WorkUnit> units;  // n_tiles sequence tiles, then the packed windows (8 per-die lists each)
-  size_t n_tiles = 0;
-  std::vector<uint64_t> window_starts;  // kWindowWords per packed window
-};
-
-UnitList build_units(const dcp_attn_desc* d, int tile, int window_tile, bool keys_major) {
-  const int32_t* cu = d->cu_seqlens_host;
-  const int32_t H = d->n_heads;
-  const int32_t n = d->n_seqs;
-  UnitList out;
-  const size_t total = tiles_per_head(d, tile) * size_t(H);
-  if (total == 0) return out;
-  const size_t cap = std::max<size_t>(4, (total + 8 * kNumXcd - 1) / (8 * kNumXcd));
-  // A chunk's work does not depend on its head, so the groups are ordered
-  // (longest first) and each expands into its H chunks; thousands of short
-  // sequences then cost a sort of the groups only.
-  struct Group {
-    int64_t work;
-    int32_t b, t_begin, t_end;
-    int32_t window;  // >= 0: packed window number (b: its first sequence, t_end: its rows)
-  };
-  std::vector<Group> groups;
-  auto tile_work = [&](int32_t len, int32_t t0, int32_t rows) -> int64_t {
-    if (!d->causal) return len;
-    return keys_major ? int64_t(len) - t0 : int64_t(t0) + rows;
-  };
-  auto add_sequence = [&](int32_t b) {
-    const int32_t len = cu[b + 1] - cu[b];
-    const int32_t nt = (len + tile - 1) / tile;
-    for (int32_t c0 = 0; c0 < nt; c0 += int32_t(cap)) {
-      Group g{0, b, c0, std::min<int32_t>(nt, c0 + int32_t(cap)), -1};
-      for (int32_t t = g.t_begin; t < g.t_end; ++t) g.work += tile_work(len, t * tile, std::min(tile, len - t * tile));
-      groups.push_back(g);
-    }
-  };
-  for (int32_t b = 0; b < n;) {
-    if (cu[b + 1] - cu[b] >= window_tile) {
-      add_sequence(b++);
-      continue;
-    }
-    // the run of short sequences from b that fits one window
-    int32_t e = b, nonempty = 0, last = b;
-    while (e < n && cu[e + 1] - cu[e] < window_tile && cu[e + 1] - cu[b] <= window_tile) {
-      if (cu[e + 1] > cu[e]) {
-        ++nonempty;
-        last = e;
-      }
-      ++e;
-    }
-    if (nonempty == 1) {
-      add_sequence(last);
-    } else if (nonempty > 1) {
-      const int32_t w = int32_t(out.window_starts.size() / kWindowWords);
-      out.window_starts.resize(out.window_starts.size() + kWindowWords, 0);
-      uint64_t* m = &out.window_starts[size_t(w) * kWindowWords];
-      const int32_t rows = cu[e] - cu[b];
-      for (int32_t i = b; i < e; ++i) {
-        const int32_t x = cu[i] - cu[b];
-        if (x < rows) m[x / 64] |= uint64_t(1) << (x % 64);
-      }
-      groups.push_back(Group{rows, b, 0, rows, w});
-    }
-    b = e;
-  }
-  std::stable_sort(groups.begin(), groups.end(), [](const Group& x, const Group& y) { return x.work > y.work; });
-  // within a chunk, the tile with the most work first (causal: the last
-  // query tiles of the forward, the first key tiles of the dK/dV pass)
-  const bool reverse = d->causal && !keys_major;
-  // sequence tiles and packed windows run as separate launches: each is
-  // balanced over the dies on its own
-  for (int windows = 0; windows < 2; ++windows) {
-    std::vector<std::vector<WorkUnit>> lists(kNumXcd);
-    for (auto& l : lists) l.reserve(total / kNumXcd + size_t(cap) + 1);
-    int64_t load[kNumXcd] = {0};
-    for (const Group& g : groups) {
-      if ((g.window >= 0) != (windows == 1)) continue;
-      const int32_t s0 = cu[g.b], len = cu[g.b + 1] - cu[g.b];
-      for (int32_t h = 0; h < H; ++h) {
-        // the least-loaded die takes the chunk
-        int x = 0;
-        for (int i = 1; i < kNumXcd; ++i)
-          if (load[i] < load[x]) x = i;
-        load[x] += g.work;
-        std::vector<WorkUnit>& l = lists[size_t(x)];
-        if (g.window >= 0) {
-          WorkUnit u{};
-          u.row0 = s0;
-          u.seq0 = s0;
-          u.seqlen = -g.window - 1;
-          u.rows = uint16_t(g.t_end);
-          u.head = uint16_t(h);
-          l.push_back(u);
-          continue;
-        }
-        for (int32_t i = g.t_begin; i < g.t_end; ++i) {
-          const int32_t t = reverse ? g.t_end - 1 - (i - g.t_begin) : i;
-          WorkUnit u{};
-          u.row0 = s0 + t * tile;
-          u.rows = uint16_t(std::min(tile, len - t * tile));
-          u.seq0 = s0;
-          u.seqlen = len;
-          u.head = uint16_t(h);
-          l.push_back(u);
-        }
-      }
-    }
-    size_t per = 0;
-    for (const auto& l : lists) per = std::max(per, l.size());
-    const size_t at = out.units.size();
-    out.units.resize(at + per * kNumXcd, WorkUnit{});
-    for (int x = 0; x < kNumXcd; ++x)
-      std::copy(lists[size_t(x)].begin(), lists[size_t(x)].end(), out.units.begin() + ptrdiff_t(at + size_t(x) * per));
-    if (windows == 0) out.n_tiles = out.units.size();
-  }
-  return out;
-}
-
-// Upper bound on build_units' length (padding included) for workspace
-// sizing: no die list is longer than the total tile count.
-size_t count_units(const dcp_attn_desc* d, int tile) {
-  return tiles_per_head(d, tile) * size_t(d->n_heads) * kNumXcd;
-}
-
-// Bytes reserved for one work list and, after it, its window masks (there
-// are fewer windows than tiles of one head).
-size_t list_bytes(const dcp_attn_desc* d, int tile) {
-  return align_up(sizeof(WorkUnit) * std::max<size_t>(1, count_units(d, tile)));
-}
-size_t window_bytes(const dcp_attn_desc* d, int tile) {
-  return align_up(sizeof(uint64_t) * kWindowWords * std::max<size_t>(1, tiles_per_head(d, tile)));
-}
-
-// Backward workspace: constant chunks | key-tile list | its window masks |
-// query-tile list | its window masks | LSE*log2e [H, T] | Delta [H, T].
-struct BwdLayout {
-  size_t units, windows, qunits, qwindows, lse2, delta, total;
-};
-BwdLayout bwd_layout(const dcp_attn_desc* d) {
-  const size_t per_row = align_up(size_t(4) * size_t(d->n_heads) * size_t(d->total_tokens));
-  const int kt = bwd_key_tile_rows(d->head_dim), qt = bwd_query_tile_rows(d->head_dim);
-  BwdLayout l;
-  l.units = kConstBytes;
-  l.windows = l.units + list_bytes(d, kt);
-  l.qunits = l.windows + window_bytes(d, kt);
-  l.qwindows = l.qunits + list_bytes(d, qt);
-  l.lse2 = l.qwindows + window_bytes(d, qt);
-  l.delta = l.lse2 + per_row;
-  l.total = l.delta + per_row;
-  return l;
-}
-
 // The constant block at the head of a workspace -- 16-byte chunks the
 // kernels' direct-to-LDS copies read for pad columns ([0 x 8] and
 // [1, 0 x 7] in bf16) and for rows past a sequence end (fp32 +inf) --
@@ -276,11 +57,8 @@ struct ListAt {
   const UnitList* list;
 };
 int upload_head(std::initializer_list<ListAt> lists, void* dst, hipStream_t stream) {
-  unsigned char head[kConstBytes] = {};
-  const uint16_t one = 0x3F80;  // bf16 1.0
-  std::memcpy(head + kConstOnes * 2, &one, sizeof one);
-  const float inf = std::numeric_limits<float>::infinity();
-  std::memcpy(head + kConstInf * 2, &inf, sizeof inf);
+  unsigned char head[kConstBytes];
+  const_head(head);
   unsigned char* base = static_cast<unsigned char*>(dst);
   hipError_t e = hipMemcpyAsync(dst, head, sizeof head, hipMemcpyHostToDevice, stream);
   for (const ListAt& l : lists) {
@@ -296,20 +74,70 @@ int upload_head(std::initializer_list<ListAt> lists, void* dst, hipStream_t stre
   return DCP_OK;
 }
 
-// Forward workspace: constant chunks | tile list | its window masks.
-size_t fwd_windows_at(const dcp_attn_desc* d) { return kConstBytes + list_bytes(d, fwd_tile_rows(d->head_dim)); }
-size_t fwd_workspace_bytes(const dcp_attn_desc* d) {
-  return fwd_windows_at(d) + window_bytes(d, fwd_tile_rows(d->head_dim));
+int check_fwd_tensors(const void* q, const void* k, const void* v, const void* o, const float* lse) {
+  int st;
+  if ((st = check_tensor(q, "q")) || (st = check_tensor(k, "k")) || (st = check_tensor(v, "v")) ||
+      (st = check_tensor(o, "o")))
+    return st;
+  if (!lse || reinterpret_cast<uintptr_t>(lse) % 4) return fail(DCP_ERR_INVALID, "lse is null or misaligned");
+  return DCP_OK;
+}
+
+int check_bwd_tensors(const void* dout, const void* o, const float* lse, const void* q, const void* k,
+                      const void* v, const void* dq, const void* dk, const void* dv) {
+  int st;
+  if ((st = check_tensor(dout, "dout")) || (st = check_tensor(o, "o")) || (st = check_tensor(q, "q")) ||
+      (st = check_tensor(k, "k")) || (st = check_tensor(v, "v")) || (st = check_tensor(dq, "dq")) ||
+      (st = check_tensor(dk, "dk")) || (st = check_tensor(dv, "dv")))
+    return st;
+  if (!lse || reinterpret_cast<uintptr_t>(lse) % 4) return fail(DCP_ERR_INVALID, "lse is null or misaligned");
+  return DCP_OK;
+}
+
+// Launches the forward over `fwd` (its units and masks already on the
+// device at ws + units_at / windows_at).
+int run_fwd(const dcp_attn_desc* d, const UnitList& fwd, const void* q, const void* k, const void* v, void* o,
+            float* lse, char* ws, size_t units_at, size_t windows_at, hipStream_t s) {
+  FwdArgs a{q, k, v, o, lse, ws, ws + units_at, ws + windows_at, int(fwd.n_tiles),
+            int(fwd.units.size() - fwd.n_tiles), d->n_heads, d->head_dim, int(d->total_tokens),
+            d->scale, d->causal, s};
+  hipError_t e = launch_fwd(a);
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "forward launch: %s", hipGetErrorString(e));
+  return DCP_OK;
+}
+
+int run_bwd(const dcp_attn_desc* d, const UnitList& kl, const UnitList& ql, const void* dout, const void* o,
+            const float* lse, const void* q, const void* k, const void* v, void* dq, void* dk, void* dv, char* ws,
+            size_t units_at, size_t windows_at, size_t qunits_at, size_t qwindows_at, size_t lse2_at,
+            size_t delta_at, hipStream_t s) {
+  BwdArgs a{dout, o, lse, q, k, v, dq, dk, dv, reinterpret_cast<float*>(ws + delta_at),
+            reinterpret_cast<float*>(ws + lse2_at), ws, ws + units_at, ws + windows_at, int(kl.n_tiles),
+            int(kl.units.size() - kl.n_tiles), ws + qunits_at, ws + qwindows_at, int(ql.n_tiles),
+            int(ql.units.size() - ql.n_tiles), d->cu_seqlens_host[d->n_seqs], d->n_heads, d->head_dim,
+            int(d->total_tokens), d->scale, d->causal, s};
+  hipError_t e = launch_bwd(a);
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "backward launch: %s", hipGetErrorString(e));
+  return DCP_OK;
+}
+
+// A batch's workspace must be the buffer its lists were uploaded into, on
+// the current device, and large enough.
+int check_batch_ws(const dcp_batch_s* b, const void* ws, size_t bytes) {
+  if (!b) return fail(DCP_ERR_INVALID, "batch is null");
+  if (!ws || bytes < b->total)
+    return fail(DCP_ERR_WORKSPACE, "batch workspace needs %zu bytes, got %zu", b->total, bytes);
+  if (ws != b->uploaded) return fail(DCP_ERR_INVALID, "workspace is not the buffer dcp_batch_upload filled");
+  int dev = -1;
+  int st = check_device(&dev);
+  if (st) return st;
+  if (dev != b->device) return fail(DCP_ERR_INVALID, "the batch was uploaded on device %d, current is %d", b->device, dev);
+  return DCP_OK;
 }
 
 }  // namespace
 }  // namespace dcp
 
 using namespace dcp;
-
-extern "C" const char* dcp_last_error(void) { return g_last_error.c_str(); }
-
-extern "C" const char* dcp_version(void) { return "dcp-mi355x 0.1 (gfx950)"; }
 
 extern "C" int dcp_set_kernel_events(void* begin, void* end) {
   clear_error();
@@ -324,7 +152,7 @@ extern "C" int dcp_varlen_attn_fwd_workspace_size(const dcp_attn_desc* desc, siz
   int st = validate_desc(desc);
   if (st) return st;
   if (!bytes) return fail(DCP_ERR_INVALID, "bytes is null");
-  *bytes = fwd_workspace_bytes(desc);
+  *bytes = fwd_layout(desc).total;
   return DCP_OK;
 }
 
@@ -342,28 +170,17 @@ extern "C" int dcp_varlen_attn_fwd(const dcp_attn_desc* desc, const void* q, con
   clear_error();
   int st = validate_desc(desc);
   if (st) return st;
-  if ((st = check_tensor(q, "q")) || (st = check_tensor(k, "k")) || (st = check_tensor(v, "v")) ||
-      (st = check_tensor(o, "o")))
-    return st;
-  if (!lse || reinterpret_cast<uintptr_t>(lse) % 4) return fail(DCP_ERR_INVALID, "lse is null or misaligned");
-  const int tile = fwd_tile_rows(desc->head_dim);
-  const size_t need = fwd_workspace_bytes(desc);
-  if (!workspace || workspace_bytes < need)
-    return fail(DCP_ERR_WORKSPACE, "forward workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if ((st = check_fwd_tensors(q, k, v, o, lse))) return st;
+  const FwdLayout l = fwd_layout(desc);
+  if (!workspace || workspace_bytes < l.total)
+    return fail(DCP_ERR_WORKSPACE, "forward workspace needs %zu bytes, got %zu", l.total, workspace_bytes);
   if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(DCP_ERR_INVALID, "workspace must be 16-byte aligned");
   if ((st = check_device())) return st;
-  const UnitList units = build_units(desc, tile, fwd_window_rows(desc->head_dim), false);
+  const UnitList units = build_pass(desc, kPassFwd);
   if (units.units.empty()) return DCP_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const size_t windows_at = fwd_windows_at(desc);
-  if ((st = upload_head({{kConstBytes, windows_at, &units}}, workspace, s))) return st;
-  char* ws = static_cast<char*>(workspace);
-  FwdArgs a{q, k, v, o, lse, ws, ws + kConstBytes, ws + windows_at, int(units.n_tiles),
-            int(units.units.size() - units.n_tiles), desc->n_heads, desc->head_dim, int(desc->total_tokens),
-            desc->scale, desc->causal, s};
-  hipError_t e = launch_fwd(a);
-  if (e != hipSuccess) return fail(DCP_ERR_HIP, "forward launch: %s", hipGetErrorString(e));
-  return DCP_OK;
+  if ((st = upload_head({{l.units, l.windows, &units}}, workspace, s))) return st;
+  return run_fwd(desc, units, q, k, v, o, lse, static_cast<char*>(workspace), l.units, l.windows, s);
 }
 
 extern "C" int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, const void* o, const float* lse,
@@ -372,33 +189,96 @@ extern "C" int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, 
   clear_error();
   int st = validate_desc(desc);
   if (st) return st;
-  if ((st = check_tensor(dout, "dout")) || (st = check_tensor(o, "o")) || (st = check_tensor(q, "q")) ||
-      (st = check_tensor(k, "k")) || (st = check_tensor(v, "v")) || (st = check_tensor(dq, "dq")) ||
-      (st = check_tensor(dk, "dk")) || (st = check_tensor(dv, "dv")))
-    return st;
-  if (!lse || reinterpret_cast<uintptr_t>(lse) % 4) return fail(DCP_ERR_INVALID, "lse is null or misaligned");
+  if ((st = check_bwd_tensors(dout, o, lse, q, k, v, dq, dk, dv))) return st;
   const BwdLayout l = bwd_layout(desc);
   if (!workspace || workspace_bytes < l.total)
     return fail(DCP_ERR_WORKSPACE, "backward workspace needs %zu bytes, got %zu", l.total, workspace_bytes);
   if (reinterpret_cast<uintptr_t>(workspace) % 16) return fail(DCP_ERR_INVALID, "workspace must be 16-byte aligned");
   if ((st = check_device())) return st;
-  const UnitList units =
-      build_units(desc, bwd_key_tile_rows(desc->head_dim), bwd_key_window_rows(desc->head_dim), true);
+  const UnitList units = build_pass(desc, kPassDkdv);
   if (units.units.empty()) return DCP_OK;
-  const UnitList qunits =
-      build_units(desc, bwd_query_tile_rows(desc->head_dim), bwd_query_window_rows(desc->head_dim), false);
+  const UnitList qunits = build_pass(desc, kPassDq);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  char* ws = static_cast<char*>(workspace);
   if ((st = upload_head({{l.units, l.windows, &units}, {l.qunits, l.qwindows, &qunits}}, workspace, s))) return st;
-  BwdArgs a{dout, o, lse, q, k, v, dq, dk, dv, reinterpret_cast<float*>(ws + l.delta),
-            reinterpret_cast<float*>(ws + l.lse2), ws, ws + l.units, ws + l.windows, int(units.n_tiles),
-            int(units.units.size() - units.n_tiles), ws + l.qunits, ws + l.qwindows, int(qunits.n_tiles),
-            int(qunits.units.size() - qunits.n_tiles),
-            desc->cu_seqlens_host[desc->n_seqs], desc->n_heads, desc->head_dim, int(desc->total_tokens),
-            desc->scale, desc->causal, s};
-  hipError_t e = launch_bwd(a);
-  if (e != hipSuccess) return fail(DCP_ERR_HIP, "backward launch: %s", hipGetErrorString(e));
+  return run_bwd(desc, units, qunits, dout, o, lse, q, k, v, dq, dk, dv, static_cast<char*>(workspace), l.units,
+                 l.windows, l.qunits, l.qwindows, l.lse2, l.delta, s);
+}
+
+// ---------------------------------------------------------------------------
+// Prepared batches.
+
+extern "C" int dcp_batch_create(const dcp_attn_desc* desc, dcp_batch* out) {
+  clear_error();
+  if (!out) return fail(DCP_ERR_INVALID, "out is null");
+  *out = nullptr;
+  dcp_batch_s* b = new (std::nothrow) dcp_batch_s();
+  if (!b) return fail(DCP_ERR_INVALID, "out of host memory");
+  int st;
+  try {
+    st = batch_init(desc, b);
+  } catch (const std::bad_alloc&) {
+    st = fail(DCP_ERR_INVALID, "out of host memory building the work lists");
+  }
+  if (st) {
+    delete b;
+    return st;
+  }
+  *out = b;
   return DCP_OK;
+}
+
+extern "C" void dcp_batch_destroy(dcp_batch b) { delete b; }
+
+extern "C" int dcp_batch_workspace_size(dcp_batch b, size_t* bytes) {
+  clear_error();
+  if (!b || !bytes) return fail(DCP_ERR_INVALID, "batch or bytes is null");
+  *bytes = b->total;
+  return DCP_OK;
+}
+
+extern "C" int dcp_batch_upload(dcp_batch b, void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  if (!b) return fail(DCP_ERR_INVALID, "batch is null");
+  if (!workspace || workspace_bytes < b->total)
+    return fail(DCP_ERR_WORKSPACE, "batch workspace needs %zu bytes, got %zu", b->total, workspace_bytes);
+  if (reinterpret_cast<uintptr_t>(workspace) % 256) return fail(DCP_ERR_INVALID, "workspace must be 256-byte aligned");
+  int dev = -1;
+  int st = check_device(&dev);
+  if (st) return st;
+  st = upload_head({{b->units_at[kPassFwd], b->windows_at[kPassFwd], &b->pass[kPassFwd]},
+                    {b->units_at[kPassDkdv], b->windows_at[kPassDkdv], &b->pass[kPassDkdv]},
+                    {b->units_at[kPassDq], b->windows_at[kPassDq], &b->pass[kPassDq]}},
+                   workspace, static_cast<hipStream_t>(stream));
+  if (st) return st;
+  b->uploaded = workspace;
+  b->device = dev;
+  return DCP_OK;
+}
+
+extern "C" int dcp_batch_fwd(dcp_batch b, const void* q, const void* k, const void* v, void* o, float* lse,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  int st = check_batch_ws(b, workspace, workspace_bytes);
+  if (st) return st;
+  if ((st = check_fwd_tensors(q, k, v, o, lse))) return st;
+  const UnitList& f = b->pass[kPassFwd];
+  if (f.units.empty()) return DCP_OK;
+  return run_fwd(&b->desc, f, q, k, v, o, lse, static_cast<char*>(workspace), b->units_at[kPassFwd],
+                 b->windows_at[kPassFwd], static_cast<hipStream_t>(stream));
+}
+
+extern "C" int dcp_batch_bwd(dcp_batch b, const void* dout, const void* o, const float* lse, const void* q,
+                             const void* k, const void* v, void* dq, void* dk, void* dv, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  clear_error();
+  int st = check_batch_ws(b, workspace, workspace_bytes);
+  if (st) return st;
+  if ((st = check_bwd_tensors(dout, o, lse, q, k, v, dq, dk, dv))) return st;
+  if (b->pass[kPassDkdv].units.empty()) return DCP_OK;
+  return run_bwd(&b->desc, b->pass[kPassDkdv], b->pass[kPassDq], dout, o, lse, q, k, v, dq, dk, dv,
+                 static_cast<char*>(workspace), b->units_at[kPassDkdv], b->windows_at[kPassDkdv],
+                 b->units_at[kPassDq], b->windows_at[kPassDq], b->lse2_at, b->delta_at,
+                 static_cast<hipStream_t>(stream));
 }
 
 extern "C" int dcp_work_list(const dcp_attn_desc* desc, int32_t pass, int32_t* units, size_t cap, size_t* n_units,
@@ -407,15 +287,8 @@ extern "C" int dcp_work_list(const dcp_attn_desc* desc, int32_t pass, int32_t* u
   int st = validate_desc(desc);
   if (st) return st;
   if (!n_units || !n_tiles || !n_windows) return fail(DCP_ERR_INVALID, "count outputs are null");
-  int tile = 0, window = 0;
-  const int D = desc->head_dim;
-  switch (pass) {
-    case 0: tile = fwd_tile_rows(D), window = fwd_window_rows(D); break;
-    case 1: tile = bwd_key_tile_rows(D), window = bwd_key_window_rows(D); break;
-    case 2: tile = bwd_query_tile_rows(D), window = bwd_query_window_rows(D); break;
-    default: return fail(DCP_ERR_INVALID, "pass must be 0 (forward), 1 (dK/dV) or 2 (dQ)");
-  }
-  const UnitList l = build_units(desc, tile, window, pass == 1);
+  if (pass < kPassFwd || pass > kPassDq) return fail(DCP_ERR_INVALID, "pass must be 0 (forward), 1 (dK/dV) or 2 (dQ)");
+  const UnitList l = build_pass(desc, pass);
   const size_t nw = l.window_starts.size() / kWindowWords;
   if (units && cap < l.units.size()) return fail(DCP_ERR_INVALID, "units holds %zu, need %zu", cap, l.units.size());
   if (window_starts && cap_windows < nw) return fail(DCP_ERR_INVALID, "window_starts holds %zu, need %zu", cap_windows, nw);
@@ -467,10 +340,12 @@ ProfLayout prof_layout(int64_t max_len, const dcp_profile_opts* o) {
   ProfLayout l;
   l.tensor = align_up(size_t(max_len) * size_t(o->n_heads) * size_t(o->head_dim) * 2);
   l.lse = align_up(size_t(max_len) * size_t(o->n_heads) * 4);
+  // a prepared batch of the longest length: its lists and scratch bound
+  // every shorter length's
   int32_t cu[2] = {0, int32_t(max_len)};
   dcp_attn_desc d{1, cu, max_len, o->n_heads, o->head_dim, 1.f, o->causal};
-  const size_t fw = fwd_workspace_bytes(&d);
-  l.ws_bytes = std::max(fw, bwd_layout(&d).total);
+  dcp_batch_s b;
+  l.ws_bytes = batch_init(&d, &b) == DCP_OK ? b.total : 0;
   l.ws_off = 8 * l.tensor + l.lse;
   l.total = l.ws_off + l.ws_bytes;
   return l;
@@ -518,9 +393,16 @@ extern "C" int dcp_profile_cost(const int64_t* lengths, int32_t n, const dcp_pro
     if (e != hipSuccess) return fail(DCP_ERR_HIP, "fill: %s", hipGetErrorString(e));
   }
   const float scale = opts->scale > 0.f ? opts->scale : 1.f / std::sqrt(float(opts->head_dim));
-  hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
+  // Per length: the work lists are built and uploaded once, before any
+  // timing; then every warm-up and timed run is enqueued back to back (the
+  // host only launches, so it stays ahead of the device) with events around
+  // the forward and the backward of each timed run, and one synchronisation
+  // at the end.  The times are device time between the events.
+  const int32_t reps = opts->reps;
+  std::vector<hipEvent_t> ev(size_t(3 * reps), nullptr);
   for (auto& e : ev) {
     if (hipEventCreate(&e) != hipSuccess) {
+      e = nullptr;
       for (auto& x : ev)
         if (x) (void)hipEventDestroy(x);
       return fail(DCP_ERR_HIP, "hipEventCreate failed");
@@ -532,28 +414,36 @@ extern "C" int dcp_profile_cost(const int64_t* lengths, int32_t n, const dcp_pro
     const int64_t len = lengths[i];
     int32_t cu[2] = {0, int32_t(len)};
     dcp_attn_desc d{1, cu, len, opts->n_heads, opts->head_dim, scale, opts->causal};
-    std::vector<float> tf, tb;
-    for (int32_t r = 0; r < opts->warmup + opts->reps && result == DCP_OK; ++r) {
-      (void)hipEventRecord(ev[0], s);
-      result = dcp_varlen_attn_fwd(&d, t[0], t[1], t[2], t[3], lse, aws, l.ws_bytes, stream);
+    dcp_batch_s b;
+    if ((result = batch_init(&d, &b))) break;
+    if (b.total > l.ws_bytes) {
+      result = fail(DCP_ERR_WORKSPACE, "length %lld needs %zu workspace bytes", static_cast<long long>(len), b.total);
+      break;
+    }
+    if ((result = dcp_batch_upload(&b, aws, l.ws_bytes, stream))) break;
+    for (int32_t r = 0; r < opts->warmup + reps && result == DCP_OK; ++r) {
+      const int32_t k = r - opts->warmup;  // timed run index (< 0: warm-up)
+      if (k >= 0) (void)hipEventRecord(ev[size_t(3 * k)], s);
+      result = dcp_batch_fwd(&b, t[0], t[1], t[2], t[3], lse, aws, l.ws_bytes, stream);
       if (result) break;
-      (void)hipEventRecord(ev[1], s);
-      result = dcp_varlen_attn_bwd(&d, t[4], t[3], lse, t[0], t[1], t[2], t[5], t[6], t[7], aws, l.ws_bytes, stream);
+      if (k >= 0) (void)hipEventRecord(ev[size_t(3 * k + 1)], s);
+      result = dcp_batch_bwd(&b, t[4], t[3], lse, t[0], t[1], t[2], t[5], t[6], t[7], aws, l.ws_bytes, stream);
       if (result) break;
-      (void)hipEventRecord(ev[2], s);
-      if (hipEventSynchronize(ev[2]) != hipSuccess) {
-        result = fail(DCP_ERR_HIP, "profile run failed: %s", hipGetErrorString(hipGetLastError()));
-        break;
-      }
-      if (r >= opts->warmup) {
-        float a = 0.f, b = 0.f;
-        (void)hipEventElapsedTime(&a, ev[0], ev[1]);
-        (void)hipEventElapsedTime(&b, ev[1], ev[2]);
-        tf.push_back(a);
-        tb.push_back(b);
-      }
+      if (k >= 0) (void)hipEventRecord(ev[size_t(3 * k + 2)], s);
     }
     if (result) break;
+    if (hipEventSynchronize(ev[size_t(3 * reps - 1)]) != hipSuccess) {
+      result = fail(DCP_ERR_HIP, "profile run failed: %s", hipGetErrorString(hipGetLastError()));
+      break;
+    }
+    std::vector<float> tf, tb;
+    for (int32_t k = 0; k < reps; ++k) {
+      float a = 0.f, c = 0.f;
+      (void)hipEventElapsedTime(&a, ev[size_t(3 * k)], ev[size_t(3 * k + 1)]);
+      (void)hipEventElapsedTime(&c, ev[size_t(3 * k + 1)], ev[size_t(3 * k + 2)]);
+      tf.push_back(a);
+      tb.push_back(c);
+    }
     std::sort(tf.begin(), tf.end());
     std::sort(tb.begin(), tb.end());
     const double mf = tf[tf.size() / 2], mb = tb[tb.size() / 2];

@@ -178,3 +178,25 @@ def test_binding_rejects_cu_seqlens_outside_int32(cu):
     from paper_2608_07524_amd._native import _host_cu
     with pytest.raises(ValueError):
         _host_cu(cu)
+
+
+def test_batch_handle_on_the_host():
+    """dcp_batch_create validates like the per-call API and sizes its buffer
+    (constants, three lists, the backward's 8*H*T bytes of scratch); a call
+    on a buffer that was never uploaded is refused before any device work."""
+    lib = P.load()
+    h = C.c_void_p()
+    d, keep = _desc([0, 5, 3], 5)
+    assert lib.dcp_batch_create(C.byref(d), C.byref(h)) == N.DCP_ERR_INVALID and not h.value
+    d, keep = _desc([0, 300, 1000], 1000, H=3, D=72, causal=1)
+    assert lib.dcp_batch_create(C.byref(d), C.byref(h)) == N.DCP_OK and h.value
+    n = C.c_size_t()
+    assert lib.dcp_batch_workspace_size(h, C.byref(n)) == N.DCP_OK
+    assert n.value >= 256 + 8 * 3 * 1000 and n.value % 256 == 0
+    assert lib.dcp_batch_fwd(h, 16, 16, 16, 16, 16, None, 0, None) == N.DCP_ERR_WORKSPACE
+    assert lib.dcp_batch_fwd(h, 16, 16, 16, 16, 16, 4096, n.value, None) == N.DCP_ERR_INVALID
+    assert "dcp_batch_upload" in N.last_error()
+    assert lib.dcp_batch_bwd(h, 16, 16, 16, 16, 16, 16, 16, 16, 16, 4096, n.value, None) == N.DCP_ERR_INVALID
+    assert lib.dcp_batch_upload(h, 4096 + 16, n.value, None) == N.DCP_ERR_INVALID  # alignment
+    lib.dcp_batch_destroy(h)
+    lib.dcp_batch_destroy(None)

@@ -51,6 +51,32 @@ def test_bitwise_deterministic(torch, D, causal, lengths):
         assert np.array_equal(x, y)
 
 
+@pytest.mark.parametrize("D,causal,lengths", [(128, True, [700, 1, 2049, 300]),
+                                              (72, False, [5, 17, 40, 3, 700, 60, 60, 1, 0, 9, 127])])
+def test_prepared_batch_equals_per_call(torch, D, causal, lengths):
+    """dcp_batch_fwd / _bwd (lists built and uploaded once) give the per-call
+    results bit for bit, on repeated calls and after uploading again into a
+    second buffer."""
+    import paper_2608_07524_amd as P
+    rng = np.random.default_rng(11)
+    cu = I.cu_from_lengths(lengths)
+    bits = I.tensors(rng, int(cu[-1]), 3, D)
+    ref = _outputs(torch, bits, cu, 1 / math.sqrt(D), causal)
+    q, k, v, do = (to_device(torch, b) for b in bits)
+    call = P.PreparedAttention(q, k, v, do, cu, 1 / math.sqrt(D), causal)
+    for rep in range(3):
+        if rep == 2:  # a second buffer
+            call.ws = torch.empty_like(call.ws)
+            P.load().dcp_batch_upload(call.batch, call.ws.data_ptr(), call.ws.numel(), call.stream)
+        for t in (call.o, call.dq, call.dk, call.dv):
+            t.zero_()
+        call.step()
+        torch.cuda.synchronize()
+        got = [to_bits(call.o), call.lse.cpu().numpy(), to_bits(call.dq), to_bits(call.dk), to_bits(call.dv)]
+        for x, y in zip(ref, got):
+            assert np.array_equal(x, y)
+
+
 @pytest.mark.parametrize("causal", [False, True])
 def test_position_in_pack_invariance(torch, causal):
     """A sequence's outputs do not depend on where it sits in the pack or
