@@ -1,15 +1,21 @@
 """Benchmark of the DCP hot path on one MI355X: packed varlen attention
-forward + backward over a synthetic video-DiT short-mix batch.
+forward + backward on the long-sequence workloads the method balances.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--extras a,b]
 
 A step is one forward and one backward pass of the whole packed batch
-(inputs already resident in HBM).  Prints ONE JSON line with the throughput
-in TFLOP/s counted over valid block-diagonal (query, key) pairs
-(fwd 4*pairs*H*D + bwd 10*pairs*H*D), the roofline of the dominant kernel
-timed live with HIP events, the padded-bucket baseline (same kernels, every
-sequence zero-padded to the batch maximum, still credited with the unpadded
-pairs) and the float64 oracle timed on a bounded sample on the host cores.
+(inputs already resident in HBM; the batch's work lists are built and
+uploaded once, before timing, through the prepared-batch calls).  Prints ONE
+JSON line: the throughput in TFLOP/s counted over valid block-diagonal
+(query, key) pairs (fwd 4*pairs*H*D + bwd 10*pairs*H*D) and as a fraction of
+the bf16 matrix peak, for the headline workload (default: one device's
+Ulysses shard of a 262,144-token sequence, 2 heads of width 128) and, as
+extra keys, the causal text pack and the short video mix; the roofline of the
+dominant kernel timed live with HIP events; the tile fill (valid pairs over
+the pairs in the 32x32 blocks the kernels multiply) and the matrix work the
+kernels execute; the padded-bucket baseline of the video mix; the float64
+oracle timed on a bounded sample on the host cores; and the plan of the tiny
+configuration on a cost table measured on this GPU.
 """
 
 from __future__ import annotations
@@ -19,6 +25,7 @@ import ctypes
 import json
 import math
 import os
+import platform
 import sys
 import time
 
@@ -30,17 +37,32 @@ if ROOT not in sys.path:
 
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak
 HBM_PEAK_GBS = 8000.0
+METRIC = "varlen attn fwd+bwd TFLOP/s (valid pairs) + % bf16 MFMA peak, 1 MI355X"
 
-# HBM bytes per launch of the dK/dV kernel from two rocprofv3 --pmc passes
-# (FETCH_SIZE x 2.000 and WRITE_SIZE x 1.000, the scales a plain device copy
-# of known size reads), per workload; valid only for the kernel sources
-# whose hash is recorded with them.
-MEASURED_TRAFFIC = {
-    "video_short": {"sources_sha256_16": "ee662c9eea106fa5", "bytes": (1127681.9 * 2.0 + 691200.5 * 1.0) * 1024},
-    "video2d_temporal": {"sources_sha256_16": "ee662c9eea106fa5",
-                         "bytes": (1069822.7 * 2.0 + 986398.7 * 1.0) * 1024},
+# Per workload, from rocprofv3 --pmc passes over `bench.py --workload W`
+# (profiles/): HBM bytes per launch of the dK/dV kernel (FETCH_SIZE scaled by
+# what the same counter reads for a direct-to-LDS copy of known size,
+# WRITE_SIZE by what it reads for that copy's stores) and the bf16 matrix
+# flops of the whole step (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512).  Valid only
+# for the kernel sources whose hash is recorded with them.
+MEASURED = {
+    "ulysses256k": {"sources_sha256_16": "932de4d4c97aa851", "dkdv_traffic_bytes": 17984391475.6,
+                    "mfma_flop_per_step": 316663643766784.0},
+    "text": {"sources_sha256_16": "932de4d4c97aa851", "dkdv_traffic_bytes": 14633186520.3,
+             "mfma_flop_per_step": 64359992655872.0},
 }
-KERNEL_SOURCES = ("attn_bwd.hip", "attn_common.h", "attn_launch.h")
+KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_common.h", "attn_launch.h", "tile_shapes.h")
+
+WORKLOADS = {
+    "ulysses256k": "Ulysses SP=8 shard, one 262,144-token sequence, H2 D128",
+    "ulysses128k": "Ulysses SP=8 shard, one 131,072-token sequence, H2 D128",
+    "text": "text-LM causal pack (log-normal documents to 262,144 tokens), H32 D128",
+    "video_short": "video-DiT short mix, 32 clips of 1k-8k tokens, H16 D72",
+    "video_long": "video-DiT long-tail pack (<= 131,072 tokens), H16 D72",
+    "video2d_spatial": "Transformer-2D spatial pack, H16 D72",
+    "video2d_temporal": "Transformer-2D temporal pack, H16 D72",
+    "tiny": "tiny pack of 4 sequences (429 tokens), H4 D64",
+}
 
 
 def kernel_sources_hash() -> str:
@@ -52,11 +74,11 @@ def kernel_sources_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload_name: str):
-    m = MEASURED_TRAFFIC.get(workload_name)
+def measured(workload_name: str, key: str):
+    m = MEASURED.get(workload_name)
     if m is None or m["sources_sha256_16"] != kernel_sources_hash():
         return None
-    return m["bytes"]
+    return m.get(key)
 
 
 def workload(name: str, seed: int = 0):
@@ -128,8 +150,9 @@ class HipEvents:
 
 
 def time_steps(torch, P, call, steps, warmup):
-    """Average ms per step plus the live-event averages of the main forward
-    and backward kernels over the timed steps."""
+    """Average ms per step (wall clock between two synchronisations) plus the
+    live-event averages of the forward kernel and of the dK/dV kernel over
+    the timed steps."""
     for _ in range(warmup):
         call.step()
     torch.cuda.synchronize()
@@ -149,36 +172,171 @@ def time_steps(torch, P, call, steps, warmup):
     return wall, fwd_ms, bwd_ms
 
 
-def cpu_baseline(w, rng_seed: int, budget_s: float = 12.0):
-    """float64 oracle (forward + backward) on whole sequences of the same
-    batch, taken in order until the time budget is spent."""
-    from oracle import attention as A
-    from paper_2608_07524_amd import inputs as I
+# ---------------------------------------------------------------------------
+# matrix work the kernels execute
+
+def padded_width(D: int) -> int:
+    """Width the products run over: the contraction and output widths are
+    padded to 16 (D = 72 runs 16x16x32 products over 80; 64 and 128 are
+    exact)."""
+    return (D + 15) // 16 * 16
+
+
+def computed_pairs(P, cu, H, D, causal, pass_):
+    """(query, key) pairs inside the 32x32 blocks one kernel pass multiplies,
+    per head: each 32-row group of a sequence tile meets the 32-row blocks of
+    its own sequence (up to the diagonal when causal); each 32-row group of a
+    packed window meets the blocks from its first row's sequence start to its
+    last row's sequence end."""
+    units, n_tiles, starts = P.work_list(cu, H, D, causal, pass_)
+    total = 0
+    for i, (row0, seq0, seqlen, rows, head) in enumerate(units.tolist()):
+        if rows == 0 or head != 0:
+            continue
+        if i < n_tiles:
+            nblk = (seqlen + 31) // 32
+            for g0 in range(0, rows, 32):
+                a = (row0 - seq0 + g0) // 32  # block index of the group's first row
+                if not causal:
+                    nb = nblk
+                elif pass_ == 1:  # key group: query blocks at or after it
+                    nb = nblk - a
+                else:  # query group: key blocks up to it
+                    nb = min(nblk, a + 1)
+                total += nb * 1024
+        else:
+            mask = starts[-seqlen - 1]
+            bits = [x for w in range(4) for x in range(64) if (int(mask[w]) >> x) & 1]
+            seq_starts = bits + [rows]
+            for g0 in range(0, rows, 32):
+                g1 = min(rows, g0 + 32) - 1
+                lo = max(s for s in seq_starts[:-1] if s <= g0)
+                hi = min(s for s in seq_starts if s > g1)
+                total += ((hi + 31) // 32 - lo // 32) * 1024
+    return total
+
+
+def matrix_work(P, w):
+    """Tile fill per pass and the matrix flops the kernels execute against
+    the algorithmic 14*pairs*H*D (products per pass: forward S and PV; dK/dV
+    pass S, dP, dV, dK; dQ pass S, dP, dQ; widths padded as the products
+    run).  Packed windows whose dQ the dK/dV launch forms (head widths <= 96)
+    skip the dQ pass; that saving is not subtracted here, so the model
+    overstates such packs' executed work."""
+    H, D, causal = w.n_heads, w.head_dim, w.causal
+    cu = w.cu_seqlens
+    pairs = pairs_of(w.lengths, causal)
+    Dp = padded_width(D)
+    out = {"valid_pairs_per_head": pairs, "padded_width": Dp}
+    executed = 0.0
+    for pass_, name, products in ((0, "fwd", 2), (1, "dkdv", 4), (2, "dq", 3)):
+        cp = computed_pairs(P, cu, H, D, causal, pass_)
+        out[f"{name}_fill"] = pairs / cp if cp else None
+        executed += 2.0 * products * cp * H * Dp
+    out["executed_flop_per_step"] = executed
+    out["algorithmic_flop_per_step"] = 14.0 * pairs * H * D
+    out["executed_over_algorithmic"] = executed / out["algorithmic_flop_per_step"]
+    out["note"] = ("fill = valid pairs / pairs in the 32x32 blocks a pass multiplies; executed = 2 x products x "
+                   "computed pairs x H x padded width, summed over the three passes (the dQ pass recomputes S and dP: "
+                   "18 products-worth per pair against the 14 of the convention)")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# baselines
+
+def cpu_info():
+    model = platform.processor() or ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        threads = os.cpu_count() or 1
-    rng = np.random.default_rng(rng_seed + 1)
-    done_pairs = 0
-    done = []
-    t_total = 0.0
-    for s in w.lengths:
-        if t_total > budget_s:
-            break
-        q, k, v, do = (I.bf16_to_f64(b) for b in I.tensors(rng, s, w.n_heads, w.head_dim))
-        cu = [0, s]
+        blas = None
+    return {"model": model, "os_cpu_count": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)),
+            "blas_threads": blas}
+
+
+def cpu_baseline(w, seed: int, budget_s: float = 20.0):
+    """The float64 oracle (forward + backward), timed on the host cores over
+    a bounded sample of the workload: whole sequences of the pack in order
+    while they fit the time budget; a pack of one sequence too long for the
+    budget (the Ulysses shard) is sampled as one sequence of the same shape
+    (heads, width, mask) whose length is the largest power of two the budget
+    allows.  The rate is then extrapolated, and labelled so, to the whole
+    step's 14*pairs*H*D."""
+    from oracle import attention as A
+    from paper_2608_07524_amd import inputs as I
+    info = cpu_info()
+    rng = np.random.default_rng(seed + 1)
+
+    def run(lengths):
+        T = int(sum(lengths))
+        q, k, v, do = (I.bf16_to_f64(b) for b in I.tensors(rng, T, w.n_heads, w.head_dim))
+        cu = I.cu_from_lengths(lengths)
         t0 = time.perf_counter()
         A.attention_forward(q, k, v, cu, w.scale, w.causal)
         A.attention_backward(do, q, k, v, cu, w.scale, w.causal)
-        t_total += time.perf_counter() - t0
-        done_pairs += pairs_of([s], w.causal)
-        done.append(s)
-    flops = 14.0 * done_pairs * w.n_heads * w.head_dim
-    return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"float64 fwd+bwd of {len(done)} whole sequences {done} of the same batch "
-                      f"({w.n_heads} heads, D={w.head_dim}) in {t_total:.1f} s"}
+        return time.perf_counter() - t0
 
+    done, t_total = [], 0.0
+    if len(w.lengths) == 1:
+        s = 2048
+        t = run([s])
+        done, t_total = [s], t
+        while t_total + t * 4 <= budget_s and 2 * s < w.lengths[0]:
+            s *= 2
+            t = run([s])
+            done.append(s)
+            t_total += t
+        sample = (f"float64 fwd+bwd of single sequences {done} at the shard's shape ({w.n_heads} heads, "
+                  f"D={w.head_dim}, {'causal' if w.causal else 'non-causal'}), {t_total:.1f} s")
+    else:
+        for s in w.lengths:
+            if t_total > budget_s:
+                break
+            t_total += run([s])
+            done.append(s)
+        sample = f"float64 fwd+bwd of the pack's first {len(done)} sequences {done[:12]}..., {t_total:.1f} s"
+    flops = 14.0 * pairs_of(done, w.causal) * w.n_heads * w.head_dim
+    rate = flops / t_total
+    full = 14.0 * pairs_of(w.lengths, w.causal) * w.n_heads * w.head_dim
+    return {"value": rate / 1e12, "unit": "TFLOP/s", "cores": info["blas_threads"] or info["affinity"],
+            "kind": "oracle", "sample": sample, "cpu": info,
+            "full_step_extrapolated_s": full / rate,
+            "extrapolation_note": "whole-step oracle time at the sample's measured rate (not measured)"}
+
+
+def padded_baseline(torch, P, w, q, k, v, do, steps, warmup, flop):
+    """Same kernels on the batch zero-padded to its longest sequence,
+    credited with the unpadded valid pairs."""
+    smax = max(w.lengths)
+    n = len(w.lengths)
+    H, D = w.n_heads, w.head_dim
+    qp, kp, vp, dop = (torch.zeros((n * smax, H, D), dtype=torch.bfloat16, device="cuda") for _ in range(4))
+    off = 0
+    for b, s in enumerate(w.lengths):
+        for src, dst in ((q, qp), (k, kp), (v, vp), (do, dop)):
+            dst[b * smax:b * smax + s] = src[off:off + s]
+        off += s
+    cu_p = np.arange(n + 1, dtype=np.int32) * smax
+    callp = P.PreparedAttention(qp, kp, vp, dop, cu_p, w.scale, w.causal)
+    ms_p, _, _ = time_steps(torch, P, callp, steps, warmup)
+    return {"value": flop / (ms_p * 1e-3) / 1e12, "ms_per_step": ms_p, "padded_to": smax,
+            "computed_pairs": pairs_of([smax] * n, w.causal),
+            "note": "same kernels, every sequence zero-padded to the batch maximum; credited with the unpadded "
+                    "valid pairs only"}
+
+
+# ---------------------------------------------------------------------------
+# roofline of the dominant kernel
 
 def dkdv_bytes(cu, H: int, D: int) -> float:
     """Algorithmic HBM bytes of the dK/dV pass: Q, K, V, dO read and dK, dV
@@ -220,7 +378,8 @@ def roofline(flop: float, nbytes: float, ms: float, traffic) -> dict:
            "bytes_convention": "6*rows*H*D*2 + 2*rows*H*4 (Q, K, V, dO, dK, dV; LSE, Delta) + rows*H*D*2 "
                                "(dQ of those windows)",
            "traffic": traffic,
-           "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)"}
+           "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE, WRITE_SIZE; scaled by a direct-to-LDS "
+                           "copy of known size)"}
     if mfma:
         a = flop / (ms * 1e-3) / 1e12
         out.update(bound="mfma", achieved=a, peak=BF16_PEAK_TFLOPS, unit="TFLOP/s", frac=a / BF16_PEAK_TFLOPS)
@@ -230,18 +389,87 @@ def roofline(flop: float, nbytes: float, ms: float, traffic) -> dict:
     return out
 
 
+def measure(torch, P, name, steps, warmup, seed, padded=False, with_fill=True):
+    """One workload: timing, kernels, roofline, fill, measured counters (and
+    for the short video mix the padded-bucket baseline)."""
+    w, rng = workload(name, seed)
+    H, D, causal = w.n_heads, w.head_dim, w.causal
+    T = w.total_tokens
+    cu = w.cu_seqlens
+    pairs = pairs_of(w.lengths, causal)
+    flop_fwd = 4.0 * pairs * H * D
+    flop_bwd = 10.0 * pairs * H * D
+    q, k, v, do = device_tensors(torch, rng, T, H, D)
+    call = P.PreparedAttention(q, k, v, do, cu, w.scale, causal)
+    ms, fwd_ms, bwd_ms = time_steps(torch, P, call, steps, warmup)
+    del call
+    value = (flop_fwd + flop_bwd) / (ms * 1e-3) / 1e12
+    flop_dkdv = 8.0 * pairs * H * D
+    win_rows, win_pairs = window_dq_part(P, cu, H, D, causal)
+    res = {
+        "value": value, "pct_bf16_peak": 100.0 * value / BF16_PEAK_TFLOPS, "ms_per_step": ms,
+        "config": {"workload": WORKLOADS[name], "n_seqs": len(w.lengths), "total_tokens": T, "heads": H,
+                   "head_dim": D, "causal": causal, "valid_pairs": pairs, "flop_per_step": flop_fwd + flop_bwd,
+                   "flop_convention": "fwd 4*pairs*H*D + bwd 10*pairs*H*D"},
+        "kernels": {"fwd_ms": fwd_ms, "fwd_tflops": flop_fwd / (fwd_ms * 1e-3) / 1e12, "bwd_dkdv_ms": bwd_ms,
+                    "bwd_dkdv_tflops": flop_dkdv / (bwd_ms * 1e-3) / 1e12, "bwd_rest_ms": ms - fwd_ms - bwd_ms},
+        "roofline": roofline(flop_dkdv + 2.0 * win_pairs * H * D, dkdv_bytes(cu, H, D) + 2.0 * win_rows * H * D,
+                             bwd_ms, measured(name, "dkdv_traffic_bytes")),
+    }
+    if with_fill:
+        mw = matrix_work(P, w)
+        counted = measured(name, "mfma_flop_per_step")
+        mw["counted_flop_per_step"] = counted
+        mw["counted_note"] = "SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 over one step (profiles/), null when stale"
+        res["matrix_work"] = mw
+    if padded and name == "video_short":
+        res["padded_baseline"] = padded_baseline(torch, P, w, q, k, v, do, steps, warmup, flop_fwd + flop_bwd)
+    del q, k, v, do
+    torch.cuda.empty_cache()
+    return w, res
+
+
+def tiny_plan(P):
+    """The tiny configuration's planner call on a cost table measured on
+    this GPU by dcp_profile_cost (4 rows at 4 heads of width 64), next to the
+    analytic table: L = 28, T_C = 100 us, M_C = 900 MiB, budget 1 GiB,
+    hidden 256, p in {1, 2, 4, 8}, b <= 64, G in [1, 4], with and without
+    the head-divisibility filter."""
+    from paper_2608_07524_amd import inputs as I
+    w = I.tiny()
+    h = 256
+    rows = P.profile_cost(w.lengths, w.n_heads, w.head_dim, causal=False, scale=w.scale, warmup=3, reps=10,
+                          act_bytes_per_token=34 * h, inp_bytes_per_token=2 * h)
+    table = [(r.seq_len, r.t_f_ns, r.t_b_ns, r.m_bytes, r.m_inp_bytes) for r in rows]
+    out = {"measured_rows": table}
+    for name, flags in (("head_filter", 0), ("no_head_filter", P.PLAN_FLAG_NO_HEAD_FILTER)):
+        t0 = time.perf_counter()
+        n_calls = 200
+        for _ in range(n_calls):
+            plan = P.plan(w.lengths, table, 28, 100_000, 900 << 20, 1 << 30, n_heads=w.n_heads, hidden=h,
+                          flags=flags)
+        us = (time.perf_counter() - t0) / n_calls * 1e6
+        out[name] = {"sp_size": plan.sp_size, "micro_batch": plan.micro_batch, "grad_accum": plan.grad_accum,
+                     "recompute_layers": plan.recompute_layers, "step_time_ns": plan.step_time_ns,
+                     "us_per_call_incl_binding": us}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="video_short")
+    ap.add_argument("--workload", default="ulysses256k", choices=sorted(WORKLOADS))
+    ap.add_argument("--extras", default="text,video_short",
+                    help="comma-separated workloads reported as extra keys ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-padded", action="store_true")
+    ap.add_argument("--no-plan", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
-                    help="also run one plain device copy of this many MiB (a known-traffic reference for "
-                         "HBM byte counters)")
+                    help="also run one direct-to-LDS device copy of this many MiB (the known-size reference for "
+                         "the HBM byte counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -256,74 +484,49 @@ def main():
     P.load()
 
     if args.copy_probe_mib:
-        src = torch.empty(args.copy_probe_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        from paper_2608_07524_amd.build import PROBE_LIB
+        probe = ctypes.CDLL(PROBE_LIB)
+        probe.dcp_probe_dma_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+        n = args.copy_probe_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
-        dst.copy_(src)
+        st = probe.dcp_probe_dma_copy(src.data_ptr(), dst.data_ptr(), n,
+                                      ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        torch.cuda.synchronize()
+        if st != 0 or not bool(torch.equal(src, dst)):
+            raise SystemExit("direct-to-LDS copy probe failed")
+        dst.copy_(src)  # a plain copy of the same size, for comparison
         torch.cuda.synchronize()
         del src, dst
 
-    w, rng = workload(args.workload, args.seed)
-    H, D, causal = w.n_heads, w.head_dim, w.causal
-    T = w.total_tokens
-    cu = w.cu_seqlens
-    pairs = pairs_of(w.lengths, causal)
-    flop_fwd = 4.0 * pairs * H * D
-    flop_bwd = 10.0 * pairs * H * D
-    q, k, v, do = device_tensors(torch, rng, T, H, D)
-    call = P.PreparedAttention(q, k, v, do, cu, w.scale, causal)
-    ms, fwd_ms, bwd_ms = time_steps(torch, P, call, args.steps, args.warmup)
-    value = (flop_fwd + flop_bwd) / (ms * 1e-3) / 1e12
-    # the dK/dV pass forms S, dP, dV and dK: 4 of the 5 backward products
-    flop_dkdv = 8.0 * pairs * H * D
-    win_rows, win_pairs = window_dq_part(P, cu, H, D, causal)
-    dkdv_tflops = flop_dkdv / (bwd_ms * 1e-3) / 1e12
-    fwd_tflops = flop_fwd / (fwd_ms * 1e-3) / 1e12
-
-    padded = None
-    if not args.no_padded and len(set(w.lengths)) > 1:
-        del call
-        smax = max(w.lengths)
-        n = len(w.lengths)
-        qp, kp, vp, dop = (torch.zeros((n * smax, H, D), dtype=torch.bfloat16, device="cuda") for _ in range(4))
-        off = 0
-        for b, s in enumerate(w.lengths):
-            for src, dst in ((q, qp), (k, kp), (v, vp), (do, dop)):
-                dst[b * smax:b * smax + s] = src[off:off + s]
-            off += s
-        cu_p = np.arange(n + 1, dtype=np.int32) * smax
-        callp = P.PreparedAttention(qp, kp, vp, dop, cu_p, w.scale, causal)
-        ms_p, _, _ = time_steps(torch, P, callp, args.steps, args.warmup)
-        padded = {"value": (flop_fwd + flop_bwd) / (ms_p * 1e-3) / 1e12, "ms_per_step": ms_p,
-                  "padded_to": smax, "computed_pairs": pairs_of([smax] * n, causal),
-                  "note": "same kernels, every sequence zero-padded to the batch maximum; credited with the "
-                          "unpadded valid pairs only"}
-        del callp, qp, kp, vp, dop
-
+    w, head = measure(torch, P, args.workload, args.steps, args.warmup, args.seed, padded=not args.no_padded)
     line = {
-        "metric": "varlen attn fwd+bwd TFLOP/s (valid pairs) + % bf16 MFMA peak, 1 MI355X",
-        "value": value,
+        "metric": METRIC,
+        "value": head["value"],
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "pct_bf16_peak": 100.0 * value / BF16_PEAK_TFLOPS,
-        "config": {"workload": w.name, "n_seqs": len(w.lengths), "total_tokens": T, "heads": H, "head_dim": D,
-                   "causal": causal, "valid_pairs": pairs, "flop_per_step": flop_fwd + flop_bwd,
-                   "flop_convention": "fwd 4*pairs*H*D + bwd 10*pairs*H*D"},
-        "kernels": {"fwd_ms": fwd_ms, "fwd_tflops": fwd_tflops, "bwd_dkdv_ms": bwd_ms, "bwd_dkdv_tflops": dkdv_tflops,
-                    "bwd_rest_ms": ms - fwd_ms - bwd_ms},
-        "roofline": roofline(flop_dkdv + 2.0 * win_pairs * H * D, dkdv_bytes(cu, H, D) + 2.0 * win_rows * H * D,
-                             bwd_ms, measured_traffic(args.workload)),
-        "padded_baseline": padded,
-        "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(w, args.seed),
+        "pct_bf16_peak": head["pct_bf16_peak"],
+        "config": head["config"],
+        "kernels": head["kernels"],
+        "roofline": head["roofline"],
+        "matrix_work": head.get("matrix_work"),
+        "padded_baseline": head.get("padded_baseline"),
     }
+    extras = {}
+    for name in [x for x in args.extras.split(",") if x and x != args.workload]:
+        _, extras[name] = measure(torch, P, name, args.steps, args.warmup, args.seed, padded=not args.no_padded)
+    line["also"] = extras
+    line["tiny_plan"] = None if args.no_plan else tiny_plan(P)
+    line["cpu_baseline"] = None if args.no_cpu_baseline else cpu_baseline(w, args.seed)
     print(json.dumps(line), flush=True)
 
 

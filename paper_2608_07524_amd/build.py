@@ -19,6 +19,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdcp.so")
+# measurement probe library (bench.py's counter calibration), not part of libdcp
+PROBE_SOURCES = ["probe/dma_copy.hip"]
+PROBE_LIB = os.path.join(PKG, "libdcp_probe.so")
 
 SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "layer.hip", "dcp_api.cpp", "dcp_error.cpp", "work_list.cpp", "dcp_plan.cpp",
            "layer_api.cpp"]
@@ -67,7 +70,27 @@ def build(verbose: bool = False, out: str = LIB, build_dir: str = BUILD_DIR) -> 
     if res.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stderr}")
     os.replace(tmp, out)
+    if out == LIB:
+        build_probe(build_dir)
     return out
+
+
+def build_probe(build_dir: str = BUILD_DIR) -> str:
+    """The measurement probes bench.py loads (libdcp_probe.so)."""
+    hipcc = _hipcc()
+    os.makedirs(build_dir, exist_ok=True)
+    objs = []
+    for src in PROBE_SOURCES:
+        obj = os.path.join(build_dir, os.path.basename(os.path.splitext(src)[0]) + ".o")
+        _compile(hipcc, src, obj)
+        objs.append(obj)
+    tmp = PROBE_LIB + ".tmp"
+    res = subprocess.run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs], capture_output=True,
+                         text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"probe link failed\n{res.stderr}")
+    os.replace(tmp, PROBE_LIB)
+    return PROBE_LIB
 
 
 if __name__ == "__main__":

@@ -118,3 +118,21 @@ def test_window_dq_accounting():
     # windows {5, 0, 7} and {1, 1, 0}; 300 runs as tiles
     cu = I.cu_from_lengths([5, 0, 7, 300, 1, 1, 0])
     assert B.window_dq_part(P, cu, 2, 72, False) == (14, 25 + 49 + 1 + 1)
+
+
+def test_computed_pairs_accounting():
+    """The bench's tile fill counts the 32x32 blocks each pass multiplies:
+    one 100-token sequence is 4 row groups x 4 blocks (16,384 pairs, 10,000
+    valid); causal, groups meet 1+2+3+4 (forward, dQ) or 4+3+2+1 (dK/dV)
+    blocks; a window of a 5- and a 7-token sequence is one group meeting one
+    block."""
+    import bench as B
+    import paper_2608_07524_amd as P
+    for pass_ in (0, 1, 2):
+        assert B.computed_pairs(P, [0, 100], 1, 64, False, pass_) == 16 * 1024
+        assert B.computed_pairs(P, [0, 100], 1, 64, True, pass_) == 10 * 1024
+        assert B.computed_pairs(P, [0, 5, 12], 2, 72, False, pass_) == 1024
+    w = I.Workload("t", [100], 1, 64, True, 0.125)
+    mw = B.matrix_work(P, w)
+    assert mw["fwd_fill"] == 5050 / 10240 and mw["dkdv_fill"] == 5050 / 10240
+    assert mw["executed_flop_per_step"] == 2.0 * (2 + 4 + 3) * 10240 * 64
