@@ -129,53 +129,77 @@ def _locate(cu, rows):
     return b
 
 
-def attention_rows(q, k, v, cu_seqlens, scale, causal, rows, heads):
+def _groups(cu, rows, heads):
+    """Sampled (row, head) pairs grouped by (sequence, head): {(b, h): indices}."""
+    seq = _locate(cu, rows)
+    groups = {}
+    for n, (h, b) in enumerate(zip(heads.tolist(), seq.tolist())):
+        groups.setdefault((b, h), []).append(n)
+    return groups
+
+
+def _scores_at(Qr, K, scale, causal, pos):
+    """Scores of query rows at sequence positions ``pos`` against every key
+    of their sequence (key j masked for query i when j > pos_i, causal)."""
+    S = scale * (Qr @ K.T)
+    if causal:
+        S = np.where(np.arange(K.shape[0])[None, :] > np.asarray(pos)[:, None], -np.inf, S)
+    return S
+
+
+def attention_rows(q, k, v, cu_seqlens, scale, causal, rows, heads, row_block=256):
     """O and LSE for the sampled (token row, head) pairs only.
 
-    Each sampled output is the definition evaluated for that one query row,
-    so the cost is O(s*D) per sample however long its sequence is.
-    Returns ``(o_rows [n, D], lse_rows [n])``.
+    Each sampled output is the definition evaluated for that one query row
+    over its full key row, so the cost is O(s*D) per sample however long its
+    sequence is (rows of one (sequence, head) are evaluated together, in
+    blocks of ``row_block``).  Returns ``(o_rows [n, D], lse_rows [n])``.
     """
     q = np.asarray(q)
     T = q.shape[0]
     cu = _check(cu_seqlens, T)
     rows = np.asarray(rows, dtype=np.int64)
     heads = np.asarray(heads, dtype=np.int64)
-    seq = _locate(cu, rows)
     o_rows = np.zeros((rows.size, q.shape[2]))
     lse_rows = np.zeros(rows.size)
-    for n, (r, h, b) in enumerate(zip(rows, heads, seq)):
+    for (b, h), idx in _groups(cu, rows, heads).items():
         s0, s1 = int(cu[b]), int(cu[b + 1])
         K = np.asarray(k[s0:s1, h], dtype=np.float64)
         V = np.asarray(v[s0:s1, h], dtype=np.float64)
-        Qr = np.asarray(q[r, h], dtype=np.float64)[None, :]
-        S = _scores(Qr, K, scale, causal, int(r) - s0)
-        L = _log_sum_exp_rows(S)
-        o_rows[n] = (np.exp(S - L[:, None]) @ V)[0]
-        lse_rows[n] = L[0]
+        idx = np.asarray(idx)
+        for c0 in range(0, idx.size, row_block):
+            sel = idx[c0:c0 + row_block]
+            Qr = np.asarray(q[rows[sel], h], dtype=np.float64)
+            S = _scores_at(Qr, K, scale, causal, rows[sel] - s0)
+            L = _log_sum_exp_rows(S)
+            o_rows[sel] = np.exp(S - L[:, None]) @ V
+            lse_rows[sel] = L
     return o_rows, lse_rows
 
 
-def attention_dq_rows(do, q, k, v, cu_seqlens, scale, causal, rows, heads):
-    """dQ for the sampled (token row, head) pairs only (row-local: O(s*D))."""
+def attention_dq_rows(do, q, k, v, cu_seqlens, scale, causal, rows, heads, row_block=256):
+    """dQ for the sampled (token row, head) pairs only (row-local: O(s*D)
+    per row, over the row's full softmax)."""
     q = np.asarray(q)
     T = q.shape[0]
     cu = _check(cu_seqlens, T)
     rows = np.asarray(rows, dtype=np.int64)
     heads = np.asarray(heads, dtype=np.int64)
-    seq = _locate(cu, rows)
     out = np.zeros((rows.size, q.shape[2]))
-    for n, (r, h, b) in enumerate(zip(rows, heads, seq)):
+    for (b, h), idx in _groups(cu, rows, heads).items():
         s0, s1 = int(cu[b]), int(cu[b + 1])
         K = np.asarray(k[s0:s1, h], dtype=np.float64)
         V = np.asarray(v[s0:s1, h], dtype=np.float64)
-        Qr = np.asarray(q[r, h], dtype=np.float64)[None, :]
-        dOr = np.asarray(do[r, h], dtype=np.float64)[None, :]
-        S = _scores(Qr, K, scale, causal, int(r) - s0)
-        P = np.exp(S - _log_sum_exp_rows(S)[:, None])
-        dP = dOr @ V.T
-        dS = P * (dP - (P * dP).sum(axis=1)[:, None])
-        out[n] = scale * (dS @ K)[0]
+        idx = np.asarray(idx)
+        for c0 in range(0, idx.size, row_block):
+            sel = idx[c0:c0 + row_block]
+            Qr = np.asarray(q[rows[sel], h], dtype=np.float64)
+            dOr = np.asarray(do[rows[sel], h], dtype=np.float64)
+            S = _scores_at(Qr, K, scale, causal, rows[sel] - s0)
+            P = np.exp(S - _log_sum_exp_rows(S)[:, None])
+            dP = dOr @ V.T
+            dS = P * (dP - (P * dP).sum(axis=1)[:, None])
+            out[sel] = scale * (dS @ K)
     return out
 
 
@@ -215,6 +239,52 @@ def attention_dkdv_rows(do, q, k, v, cu_seqlens, scale, causal, rows, heads, row
             dS = P * (dP - (P * dP).sum(axis=1)[:, None])
             dVc += P[:, cols].T @ dO[r0:r1]
             dKc += scale * (dS[:, cols].T @ Q[r0:r1])
+        dk_rows[idx] = dKc
+        dv_rows[idx] = dVc
+    return dk_rows, dv_rows
+
+
+def attention_dkdv_cols_given(do, q, k, v, cu_seqlens, scale, causal, rows, heads, lse, delta,
+                              row_block=16384):
+    """dK and dV for sampled (key row, head) pairs, given each query's LSE
+    ([H, T]) and Delta_i = sum_j P_ij dP_ij ([H, T]) instead of recomputing
+    them:
+        P_ij  = exp(scale q_i . k_j - LSE_i)   (0 where j > i, causal)
+        dV_j  = sum_i P_ij dO_i
+        dK_j  = scale sum_i P_ij (dO_i . v_j - Delta_i) q_i
+    the same definition with the row normalisers supplied.  The cost is
+    O(s*D) per key, so key columns of sequences too long for the full-row
+    evaluation of attention_dkdv_rows can be checked.  With the exact LSE
+    and Delta it equals attention_dkdv_rows; given approximate ones the
+    result moves by the same relative amount (|dP/P| = |dLSE|).
+    Returns ``(dk_rows [n, D], dv_rows [n, D])``."""
+    q = np.asarray(q)
+    T = q.shape[0]
+    cu = _check(cu_seqlens, T)
+    rows = np.asarray(rows, dtype=np.int64)
+    heads = np.asarray(heads, dtype=np.int64)
+    dk_rows = np.zeros((rows.size, q.shape[2]))
+    dv_rows = np.zeros((rows.size, q.shape[2]))
+    for (b, h), idx in _groups(cu, rows, heads).items():
+        s0, s1 = int(cu[b]), int(cu[b + 1])
+        idx = np.asarray(idx)
+        cols = rows[idx] - s0
+        Kc = np.asarray(k[rows[idx], h], dtype=np.float64)
+        Vc = np.asarray(v[rows[idx], h], dtype=np.float64)
+        dKc = np.zeros((cols.size, Kc.shape[1]))
+        dVc = np.zeros((cols.size, Kc.shape[1]))
+        for r0 in range(0, s1 - s0, row_block):
+            r1 = min(s1 - s0, r0 + row_block)
+            Qb = np.asarray(q[s0 + r0:s0 + r1, h], dtype=np.float64)
+            dOb = np.asarray(do[s0 + r0:s0 + r1, h], dtype=np.float64)
+            Lb = np.asarray(lse[h, s0 + r0:s0 + r1], dtype=np.float64)
+            Db = np.asarray(delta[h, s0 + r0:s0 + r1], dtype=np.float64)
+            P = np.exp(scale * (Qb @ Kc.T) - Lb[:, None])
+            if causal:
+                P = np.where(cols[None, :] > np.arange(r0, r1)[:, None], 0.0, P)
+            dS = P * (dOb @ Vc.T - Db[:, None])
+            dVc += P.T @ dOb
+            dKc += scale * (dS.T @ Qb)
         dk_rows[idx] = dKc
         dv_rows[idx] = dVc
     return dk_rows, dv_rows

@@ -228,6 +228,36 @@ def test_sampled_rows_match_full_outputs():
         assert np.max(np.abs(dv_r - dv[rows, heads])) < 1e-12
 
 
+def test_grouped_rows_and_given_normalisers():
+    """Rows of one (sequence, head) evaluated in blocks give the full
+    outputs; key columns from the supplied LSE and Delta = rowsum(dO o O)
+    equal the full backward, and shifting every LSE by e (Delta kept)
+    scales P, hence dV and dS and dK, by exp(-e)."""
+    rng = np.random.default_rng(32)
+    lens = [40, 1, 70, 0, 33]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T, H, D = int(cu[-1]), 3, 5
+    q, k, v, do = (_rand(rng, T, H, D) for _ in range(4))
+    for causal in (False, True):
+        o, lse = A.attention_forward(q, k, v, cu, 0.4, causal)
+        dq, dk, dv = A.attention_backward(do, q, k, v, cu, 0.4, causal)
+        rows = rng.integers(0, T, 60)
+        heads = rng.integers(0, H, 60)
+        o_r, l_r = A.attention_rows(q, k, v, cu, 0.4, causal, rows, heads, row_block=3)
+        assert np.max(np.abs(o_r - o[rows, heads])) < 1e-13 and np.max(np.abs(l_r - lse[heads, rows])) < 1e-13
+        dq_r = A.attention_dq_rows(do, q, k, v, cu, 0.4, causal, rows, heads, row_block=5)
+        assert np.max(np.abs(dq_r - dq[rows, heads])) < 1e-12
+        delta = np.einsum("thd,thd->ht", do, o)
+        dk_c, dv_c = A.attention_dkdv_cols_given(do, q, k, v, cu, 0.4, causal, rows, heads, lse, delta, row_block=7)
+        assert np.max(np.abs(dk_c - dk[rows, heads])) < 1e-12
+        assert np.max(np.abs(dv_c - dv[rows, heads])) < 1e-12
+        e = 0.01
+        dk_s, dv_s = A.attention_dkdv_cols_given(do, q, k, v, cu, 0.4, causal, rows, heads, lse + e, delta,
+                                                 row_block=7)
+        assert np.max(np.abs(dv_s - np.exp(-e) * dv[rows, heads])) < 1e-12
+        assert np.max(np.abs(dk_s - np.exp(-e) * dk[rows, heads])) < 1e-12
+
+
 def test_valid_pairs():
     assert A.valid_pairs([0, 37, 101, 229, 429]) == 37 ** 2 + 64 ** 2 + 128 ** 2 + 200 ** 2
     assert A.valid_pairs([0, 3, 3, 5], causal=True) == 6 + 0 + 3
