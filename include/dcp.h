@@ -127,6 +127,26 @@ int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, const void*
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Forward for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * dcp_varlen_attn_fwd without a workspace argument.  Its scratch -- the
+ * constant chunks, the tile list and the window masks -- lives in a fixed
+ * device array of the library, 8 MiB (8,388,608 bytes) per GPU, held until
+ * the process ends; the call itself allocates nothing (no hipMalloc, no
+ * allocating library routine).  The caller still passes q, k, v, o and lse.
+ *   Errors: as dcp_varlen_attn_fwd, plus DCP_ERR_WORKSPACE when the batch's
+ *   list needs more than 8 MiB (about 520,000 tiles of 256 query rows:
+ *   tiles x heads), reported on the host before anything is enqueued.
+ *   Sharing: every call on one GPU uses that GPU's single array, and each
+ *   call rewrites it (enqueued on `stream`), so calls whose work may overlap
+ *   in time -- on different streams, or from different threads without
+ *   ordering -- race; order them on one stream or by synchronisation.
+ * Outputs equal dcp_varlen_attn_fwd's bit for bit (same kernels, same list).
+ */
+int dcp_varlen_attn_fwd_noalloc(const dcp_attn_desc* desc, const void* q, const void* k, const void* v, void* o,
+                                float* lse, void* stream);
+
+/*
  * Prepared batches.  A training step runs the forward and the backward of
  * the same packed batch, and a profiler or benchmark runs them many times:
  * the tile lists of the three kernel passes (forward, dK/dV, dQ) depend only

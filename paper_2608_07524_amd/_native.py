@@ -113,6 +113,7 @@ def load() -> C.CDLL:
         "dcp_varlen_attn_fwd": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp, sz, vp], C.c_int),
         "dcp_varlen_attn_bwd": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], C.c_int),
         "dcp_set_kernel_events": ([vp, vp], C.c_int),
+        "dcp_varlen_attn_fwd_noalloc": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp], C.c_int),
         "dcp_batch_create": ([C.POINTER(AttnDesc), C.POINTER(vp)], C.c_int),
         "dcp_batch_workspace_size": ([vp, C.POINTER(sz)], C.c_int),
         "dcp_batch_upload": ([vp, vp, sz, vp], C.c_int),
@@ -255,6 +256,23 @@ def varlen_attn_fwd(q, k, v, cu_seqlens, scale: Optional[float] = None, causal: 
     ws = torch.empty(n.value, dtype=torch.uint8, device=q.device) if workspace is None else workspace
     _check(lib.dcp_varlen_attn_fwd(d.ref, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
                                    ws.data_ptr(), _nbytes(ws), _stream_ptr(torch, q.device)))
+    return o, lse
+
+
+def varlen_attn_fwd_noalloc(q, k, v, cu_seqlens, scale: Optional[float] = None, causal: bool = False,
+                            out=None, lse=None):
+    """O, LSE through dcp_varlen_attn_fwd_noalloc (the library's fixed
+    scratch instead of a workspace; pass ``out`` and ``lse`` to allocate
+    nothing here either)."""
+    import torch
+    given = [("k", k), ("v", v)] + ([("out", out)] if out is not None else [])
+    T, H, D = _check_attn(torch, q, given, lse)
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    d = _Desc(_host_cu(cu_seqlens), T, H, D, scale, causal)
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty((H, T), dtype=torch.float32, device=q.device) if lse is None else lse
+    _check(load().dcp_varlen_attn_fwd_noalloc(d.ref, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                              lse.data_ptr(), _stream_ptr(torch, q.device)))
     return o, lse
 
 

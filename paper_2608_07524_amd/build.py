@@ -24,7 +24,7 @@ PROBE_SOURCES = ["probe/dma_copy.hip"]
 PROBE_LIB = os.path.join(PKG, "libdcp_probe.so")
 
 SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "layer.hip", "dcp_api.cpp", "dcp_error.cpp", "work_list.cpp", "dcp_plan.cpp",
-           "layer_api.cpp"]
+           "layer_api.cpp", "noalloc.hip"]
 
 # Packed fp32 vector ops stay disabled for device code (plain scalar fp32
 # VALU only); the host pass reports the feature as unknown, which is benign.

@@ -12,6 +12,7 @@
 
 #include "attn_common.h"
 #include "attn_launch.h"
+#include "api_internal.h"
 #include "dcp_internal.h"
 #include "work_list.h"
 
@@ -22,10 +23,8 @@ KernelEvents& kernel_events() {
   return ev;
 }
 
-namespace {
-
 // The kernels are built for gfx950 only; refuse other devices up front.
-int check_device(int* device = nullptr) {
+int check_device(int* device) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "no HIP device: %s", hipGetErrorString(e));
@@ -52,10 +51,6 @@ int check_device(int* device = nullptr) {
 // and each work list with its window masks, copied to their byte offsets
 // in the workspace (one copy per array: the space reserved between them
 // is not touched).
-struct ListAt {
-  size_t units_at, windows_at;
-  const UnitList* list;
-};
 int upload_head(std::initializer_list<ListAt> lists, void* dst, hipStream_t stream) {
   unsigned char head[kConstBytes];
   const_head(head);
@@ -119,6 +114,8 @@ int run_bwd(const dcp_attn_desc* d, const UnitList& kl, const UnitList& ql, cons
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "backward launch: %s", hipGetErrorString(e));
   return DCP_OK;
 }
+
+namespace {
 
 // A batch's workspace must be the buffer its lists were uploaded into, on
 // the current device, and large enough.

@@ -200,3 +200,17 @@ def test_batch_handle_on_the_host():
     assert lib.dcp_batch_upload(h, 4096 + 16, n.value, None) == N.DCP_ERR_INVALID  # alignment
     lib.dcp_batch_destroy(h)
     lib.dcp_batch_destroy(None)
+
+
+def test_noalloc_forward_rejects_oversize_lists_on_the_host():
+    """dcp_varlen_attn_fwd_noalloc refuses a batch whose tile list exceeds
+    its fixed 8 MiB scratch before any device call (65,535 heads x 16 tiles
+    of 256 rows = 1,048,560 tiles x 16 bytes)."""
+    lib = P.load()
+    d, keep = _desc([0, 4096], 4096, H=65535, D=128)
+    st = lib.dcp_varlen_attn_fwd_noalloc(C.byref(d), 16, 16, 16, 16, 16, None)
+    assert st == N.DCP_ERR_WORKSPACE and "8388608" in N.last_error()
+    d, keep = _desc([0, 5, 3], 5)
+    assert lib.dcp_varlen_attn_fwd_noalloc(C.byref(d), 16, 16, 16, 16, 16, None) == N.DCP_ERR_INVALID
+    d, keep = _desc([0, 5], 5)
+    assert lib.dcp_varlen_attn_fwd_noalloc(C.byref(d), None, 16, 16, 16, 16, None) == N.DCP_ERR_INVALID
