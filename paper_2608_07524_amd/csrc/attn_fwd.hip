@@ -231,11 +231,18 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
 #pragma unroll
   for (int mb = 0; mb < NMB; ++mb) oacc16[mb][0] = oacc16[mb][1] = f32x4{};
 
-  // S^T of one 32-key block whose K rows start at LDS element kbase.
-  auto scores = [&](unsigned kbase) DCP_INLINE {
+  // K fragments (A operand of S^T) of one 32-key block whose K rows start
+  // at LDS element kbase, and S^T from fragments held in registers.  The
+  // fragments of the next block are read one step ahead, so the score
+  // products never wait on their LDS reads.
+  auto load_k = [&](unsigned kbase, bf16x8 (&kf)[NKD]) DCP_INLINE {
+#pragma unroll
+    for (int kd = 0; kd < NKD; ++kd) kf[kd] = lds_read_b128(Ks3 + kbase + 16 * kd);
+  };
+  auto scores = [&](const bf16x8 (&kf)[NKD]) DCP_INLINE {
     f32x16 s = f32x16{};
 #pragma unroll
-    for (int kd = 0; kd < NKD; ++kd) s = mfma32(lds_read_b128(Ks3 + kbase + 16 * kd), qf[kd], s);
+    for (int kd = 0; kd < NKD; ++kd) s = mfma32(kf[kd], qf[kd], s);
     return s;
   };
   auto apply_mask = [&](f32x16& s, int b) DCP_INLINE {
@@ -326,21 +333,27 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   for (; kt < t_first; ++kt) idle(kt);
 
   f32x16 sc{};  // S^T of the current block, masked, not yet exponentiated
+  bf16x8 kn[NKD];  // K fragments of the block after it
   if (nb > b_first) {
     unsigned kb0 = (unsigned(t_first) % NST) * KBUF + kr_off;
     asm("" : "+v"(kb0));
-    sc = scores(kb0);
+    load_k(kb0, kn);
+    sc = scores(kn);
+    load_k(kb0 + 32 * KSTR, kn);
     if (b_mask <= b_first) apply_mask(sc, b_first);
     rescale(row_max(sc), true);
   }
 
   // One pipelined step: P and O for the current block (V rows at vcur)
-  // while the scores of block bn (K rows at knext) are computed, masked
-  // when MASK, and their row max taken.  On a wavefront's last block the
-  // successor's scores are computed but not used (valid_next false).
-  auto step = [&](int bn, unsigned knext, unsigned vcur, bool valid_next, auto mask_tag) DCP_INLINE {
+  // while the scores of block bn (K fragments already in kn) are computed,
+  // masked when MASK, and their row max taken; kn then receives the K
+  // fragments of block bn + 1 (K rows at kafter).  On a wavefront's last
+  // block the successor's scores are computed but not used (valid_next
+  // false), and the reads ahead stay inside the ring.
+  auto step = [&](int bn, unsigned kafter, unsigned vcur, bool valid_next, auto mask_tag) DCP_INLINE {
     constexpr bool MASK = decltype(mask_tag)::value;
-    f32x16 sn = scores(knext);
+    f32x16 sn = scores(kn);
+    load_k(kafter, kn);
     // P = exp2(S*scale*log2e - m) as bf16 (B operand of the PV product)
     const float mneg = -m_use;
     bf16x8 pb[2];
@@ -368,15 +381,16 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
   };
 
   // Tile kt: blocks 2kt and 2kt + 1; the successor of the second block is
-  // the first block of tile kt + 1.
+  // the first block of tile kt + 1, and the reads ahead take the two blocks
+  // of tile kt + 1 (landed before tile kt began).
   auto tile = [&](int kt, auto mask_tag) DCP_INLINE {
     if (kt + PD < n_tiles) issue_tile(kt + PD);
     unsigned kb0 = (unsigned(kt) % NST) * KBUF + kr_off;
     unsigned kb1 = (unsigned(kt + 1) % NST) * KBUF + kr_off;
     unsigned vb0 = (unsigned(kt) % NST) * VBUF + tr_lane;
     asm("" : "+v"(kb0), "+v"(kb1), "+v"(vb0));  // keeps the constant terms in the offset fields
-    step(2 * kt + 1, kb0 + 32 * KSTR, vb0, 2 * kt + 1 < 2 * t_work, mask_tag);
-    step(2 * kt + 2, kb1, vb0 + 32 * VSTR + 2 * S::VSKEW, 2 * kt + 2 < 2 * t_work, mask_tag);
+    step(2 * kt + 1, kb1, vb0, 2 * kt + 1 < 2 * t_work, mask_tag);
+    step(2 * kt + 2, kb1 + 32 * KSTR, vb0 + 32 * VSTR + 2 * S::VSKEW, 2 * kt + 2 < 2 * t_work, mask_tag);
     wait_for(kt + 1);
     __syncthreads();
   };
