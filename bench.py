@@ -389,6 +389,44 @@ def roofline(flop: float, nbytes: float, ms: float, traffic) -> dict:
     return out
 
 
+def host_us_per_call(torch, P, w, call, n: int = 5):
+    """Host time of one call, averaged over n enqueued calls (the device is
+    idle at the start and the calls do not wait for it): the per-call API
+    (dcp_varlen_attn_fwd / _bwd build the work lists on the host and copy
+    them to the device each time) against the prepared batch
+    (dcp_batch_fwd / _bwd only launch)."""
+    import ctypes as C
+    from paper_2608_07524_amd import _native as N
+    lib = P.load()
+    T, H, D = w.total_tokens, w.n_heads, w.head_dim
+    d = N._Desc(w.cu_seqlens, T, H, D, w.scale, w.causal)
+    nf, nb = C.c_size_t(), C.c_size_t()
+    lib.dcp_varlen_attn_fwd_workspace_size(d.ref, C.byref(nf))
+    lib.dcp_varlen_attn_bwd_workspace_size(d.ref, C.byref(nb))
+    ws_f = torch.empty(max(1, nf.value), dtype=torch.uint8, device="cuda")
+    ws_b = torch.empty(max(1, nb.value), dtype=torch.uint8, device="cuda")
+    s = call.stream
+    a = (call.q.data_ptr(), call.k.data_ptr(), call.v.data_ptr(), call.o.data_ptr(), call.lse.data_ptr())
+    g = (call.dout.data_ptr(), call.o.data_ptr(), call.lse.data_ptr(), call.q.data_ptr(), call.k.data_ptr(),
+         call.v.data_ptr(), call.dq.data_ptr(), call.dk.data_ptr(), call.dv.data_ptr())
+    runs = {
+        "per_call_fwd": lambda: lib.dcp_varlen_attn_fwd(d.ref, *a, ws_f.data_ptr(), ws_f.numel(), s),
+        "per_call_bwd": lambda: lib.dcp_varlen_attn_bwd(d.ref, *g, ws_b.data_ptr(), ws_b.numel(), s),
+        "batch_fwd": lambda: lib.dcp_batch_fwd(call.batch, *a, call.ws.data_ptr(), call.ws.numel(), s),
+        "batch_bwd": lambda: lib.dcp_batch_bwd(call.batch, *g, call.ws.data_ptr(), call.ws.numel(), s),
+    }
+    out = {}
+    for key, fn in runs.items():
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(n):
+            if fn() != 0:
+                raise RuntimeError(N.last_error())
+        out[key] = (time.perf_counter() - t0) / n * 1e6
+        torch.cuda.synchronize()
+    return out
+
+
 def measure(torch, P, name, steps, warmup, seed, padded=False, with_fill=True):
     """One workload: timing, kernels, roofline, fill, measured counters (and
     for the short video mix the padded-bucket baseline)."""
@@ -402,6 +440,7 @@ def measure(torch, P, name, steps, warmup, seed, padded=False, with_fill=True):
     q, k, v, do = device_tensors(torch, rng, T, H, D)
     call = P.PreparedAttention(q, k, v, do, cu, w.scale, causal)
     ms, fwd_ms, bwd_ms = time_steps(torch, P, call, steps, warmup)
+    host = host_us_per_call(torch, P, w, call)
     del call
     value = (flop_fwd + flop_bwd) / (ms * 1e-3) / 1e12
     flop_dkdv = 8.0 * pairs * H * D
@@ -415,6 +454,7 @@ def measure(torch, P, name, steps, warmup, seed, padded=False, with_fill=True):
                     "bwd_dkdv_tflops": flop_dkdv / (bwd_ms * 1e-3) / 1e12, "bwd_rest_ms": ms - fwd_ms - bwd_ms},
         "roofline": roofline(flop_dkdv + 2.0 * win_pairs * H * D, dkdv_bytes(cu, H, D) + 2.0 * win_rows * H * D,
                              bwd_ms, measured(name, "dkdv_traffic_bytes")),
+        "host_us_per_call": host,
     }
     if with_fill:
         mw = matrix_work(P, w)
@@ -519,6 +559,7 @@ def main():
         "kernels": head["kernels"],
         "roofline": head["roofline"],
         "matrix_work": head.get("matrix_work"),
+        "host_us_per_call": head.get("host_us_per_call"),
         "padded_baseline": head.get("padded_baseline"),
     }
     extras = {}

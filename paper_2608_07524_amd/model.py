@@ -106,14 +106,15 @@ class Stack:
 
 
 def profile_rows(lengths: Sequence[int], n_heads: int, head_dim: int, causal: bool, reps: int = 5,
-                 warmup: int = 2) -> List[N.CostRow]:
+                 warmup: int = 2, cu_seqlens=None) -> List[N.CostRow]:
     """Dual-layer profile per length (one sequence of that length, micro-batch
-    1): the second layer's median forward and backward times, its stash bytes
+    1; or, with ``cu_seqlens``, that packed batch of ``lengths[0]`` tokens):
+    the second layer's median forward and backward times, its stash bytes
     and its input bytes."""
     import torch
     rows = []
     for s in lengths:
-        st = Stack(2, [0, int(s)], n_heads, head_dim, causal)
+        st = Stack(2, [0, int(s)] if cu_seqlens is None else cu_seqlens, n_heads, head_dim, causal)
         ev = lambda: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(2)]
         tf, tb = [], []
         for r in range(warmup + reps):

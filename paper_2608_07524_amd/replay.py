@@ -13,10 +13,10 @@ together on the second of two layers, m = that layer's stash bytes):
   heads of width 64); Transformer-2D rows time the forward and backward of a
   clip's spatial pack (f frames of n tokens) plus its temporal pack (n
   sequences of f tokens), 16 heads of width 72;
-* the rest of a layer, measured: the four projection GEMMs of one layer
-  (QKV, output, MLP up and down, hidden h, MLP 4h) timed with torch.matmul
-  on 16k tokens give picoseconds per token forward; backward takes twice
-  that (two GEMMs per forward GEMM);
+* the rest of a layer, measured through the library: its whole layer
+  (norms, projections, MLP; dcp_layer_fwd / dcp_layer_bwd) minus its
+  attention, on a batch of 128 sequences of 128 tokens (attention a small
+  share), gives picoseconds per token forward and backward;
 * memory, analytic: 34*h bytes of stashed activations per token and layer
   with flash attention (Korthikanti et al., cited in Sec. 5) and 2*h bytes
   of layer input; model states M_C = 4 bytes per parameter (bf16 weights and
@@ -53,27 +53,20 @@ def _events(torch):
     return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
 
-def gemm_ps_per_token(torch, h: int, tokens: int = 16384, reps: int = 10) -> int:
-    """Forward time per token of one layer's projection GEMMs, in ps."""
-    x = torch.randn(tokens, h, dtype=torch.bfloat16, device="cuda")
-    w = [torch.randn(h, n, dtype=torch.bfloat16, device="cuda") for n in (3 * h, h, 4 * h)]
-    w_down = torch.randn(4 * h, h, dtype=torch.bfloat16, device="cuda")
-    u = torch.randn(tokens, 4 * h, dtype=torch.bfloat16, device="cuda")
-
-    def layer():
-        for m in w:
-            torch.matmul(x, m)
-        torch.matmul(u, w_down)
-
-    for _ in range(3):
-        layer()
-    a, b = _events(torch)
-    a.record()
-    for _ in range(reps):
-        layer()
-    b.record()
-    torch.cuda.synchronize()
-    return int(a.elapsed_time(b) / reps * 1e9 / tokens)
+def layer_rest_ps_per_token(torch, P, H: int, D: int, causal: bool, n_seqs: int = 128, s: int = 128,
+                            reps: int = 5):
+    """Forward and backward time per token of one layer apart from its
+    attention, in ps: the library's whole layer (norms, projections, MLP,
+    dcp_layer_fwd / dcp_layer_bwd with a stash) minus the library's
+    attention on the same packed batch, both timed on the second of two
+    layers.  The batch is many short sequences (n_seqs x s tokens), so the
+    attention is a small share and the difference is the per-token part."""
+    from .model import profile_rows
+    cu = I.cu_from_lengths([s] * n_seqs)
+    T = int(cu[-1])
+    layer = profile_rows([T], H, D, causal, reps=reps, cu_seqlens=cu)[0]
+    af, ab = _attn_time_ns(torch, P, [s] * n_seqs, H, D, causal, reps=reps)
+    return max(0, (layer.t_f_ns - af) * 1000 // T), max(0, (layer.t_b_ns - ab) * 1000 // T)
 
 
 def _attn_time_ns(torch, P, lengths: List[int], H: int, D: int, causal: bool, reps: int = 5):
@@ -101,8 +94,7 @@ def _attn_time_ns(torch, P, lengths: List[int], H: int, D: int, causal: bool, re
 
 def cost_rows(torch, P, model: str, lengths, clips=None):
     L, h, H, D, params, causal = MODELS[model]
-    lin_f = gemm_ps_per_token(torch, h)
-    lin_b = 2 * lin_f
+    lin_f, lin_b = layer_rest_ps_per_token(torch, P, H, D, causal)
     act, inp = 34 * h, 2 * h
     rows = []
     if clips is None:
@@ -189,7 +181,7 @@ def main(argv=None):
             s = {k: _summary(v, W) for k, v in out.items()}
             base = s["bucket"]["tokens_per_s"]
             rec = {"model": model, "data": data, "budget_gib": budget_gib, "devices": W, "sync_ms": sync / 1e6,
-                   "gemm_ps_per_token_fwd": lin, "schedules": s,
+                   "layer_rest_ps_per_token_fwd": lin, "schedules": s,
                    "speedup": {k: v["tokens_per_s"] / base for k, v in s.items()}}
             results.append(rec)
             print(json.dumps(rec), flush=True)
