@@ -327,8 +327,11 @@ extern "C" int dcp_plan(const int64_t* seq_lens, int32_t n_seqs, const int32_t* 
 // imbalance ratio, the share of device time spent waiting).
 //
 // DCP: every batch takes the planner's (p_i, b_i, r_i, T_i); batches join
-// the current iteration in stream order while sum_i p_i <= W (Eq. (1)'s
-// constraint; devices left over wait out the iteration); the iteration's
+// the current iteration in stream order while they fit the devices left
+// (Eq. (1)'s sum_i p_i <= W): of the first kSimWindow batches not yet
+// placed, each that fits joins the iteration and each that does not waits
+// for a later one, keeping its place in the stream (devices still left over
+// wait out the iteration); the iteration's
 // accumulation steps g_i follow Eq. (3) with the bounds of Appendix C.
 // Bucket parallelism (Sec. 4.1 baseline, Sec. 2.4): one fixed p for every
 // batch, floor(W/p) batches per iteration in stream order, no accumulation,
@@ -339,6 +342,9 @@ extern "C" int dcp_plan(const int64_t* seq_lens, int32_t n_seqs, const int32_t* 
 // p_i*g_i*T_i, tokens sum_i g_i*b_i*S_i, time = makespan + sync.
 
 namespace {
+
+// batches an iteration looks at when filling its devices
+constexpr int64_t kSimWindow = 64;
 
 int sim_dcp(const std::vector<Unit>& units, const dcp_cost_table* t, int64_t budget, const dcp_plan_opts& o,
             int64_t W, int64_t sync, dcp_sim_result* res) {
@@ -351,27 +357,40 @@ int sim_dcp(const std::vector<Unit>& units, const dcp_cost_table* t, int64_t bud
     if (ch[i].T == 0) return dcp::fail(DCP_ERR_TABLE, "a batch has zero step time; the cost table is empty of cost");
   }
   *res = dcp_sim_result{};
-  size_t i = 0;
-  while (i < n) {
-    size_t j = i;
+  // batches not yet placed, in stream order
+  std::vector<size_t> pending(n), rest;
+  for (size_t i = 0; i < n; ++i) pending[i] = i;
+  std::vector<size_t> members;
+  while (!pending.empty()) {
+    members.clear();
+    rest.clear();
     int64_t used = 0;
-    while (j < n && used + ch[j].p <= W) used += ch[j++].p;
-    std::vector<int64_t> T(j - i), g;
-    for (size_t k = i; k < j; ++k) T[k - i] = ch[k].T;
+    for (size_t x = 0; x < pending.size(); ++x) {
+      const size_t k = pending[x];
+      if (x < size_t(kSimWindow) && used + ch[k].p <= W) {
+        members.push_back(k);
+        used += ch[k].p;
+      } else {
+        rest.push_back(k);
+      }
+    }
+    pending.swap(rest);
+    std::vector<int64_t> T(members.size()), g;
+    for (size_t m = 0; m < members.size(); ++m) T[m] = ch[members[m]].T;
     int64_t idle = 0, span = 0;
     int st = accumulate(T, o.g_min, o.g_max, &g, &idle, &span);
     if (st != DCP_OK) return st;
     i128 busy = 0, tokens = 0;
-    for (size_t k = i; k < j; ++k) {
-      busy += i128(ch[k].p) * g[k - i] * ch[k].T;
-      tokens += i128(g[k - i]) * ch[k].b * units[k].tokens;
+    for (size_t m = 0; m < members.size(); ++m) {
+      const size_t k = members[m];
+      busy += i128(ch[k].p) * g[m] * ch[k].T;
+      tokens += i128(g[m]) * ch[k].b * units[k].tokens;
     }
     res->iterations += 1;
     res->makespan_ns = chk(i128(res->makespan_ns) + span);
     res->time_ns = chk(i128(res->time_ns) + span + sync);
     res->busy_device_ns = chk(i128(res->busy_device_ns) + busy);
     res->tokens = chk(i128(res->tokens) + tokens);
-    i = j;
   }
   return DCP_OK;
 }

@@ -120,3 +120,20 @@ def test_errors():
     with pytest.raises(D.DCPError) as e:  # beyond the table
         D.simulate([101], rows, 1, 0, 0, 1 << 40, 4)
     assert e.value.code == D.DCP_ERR_TABLE
+
+
+def test_window_fill_hand_worked():
+    """Iterations fill their devices from the next batches that fit.  One
+    layer, no communication cost, budget 10: a 100-token batch (m_inp 20)
+    needs p = 2 (ceil(20/2) = 10), a 200-token batch (m_inp 40) p = 4; step
+    times T = ceil(t_f/p) + ceil(t_b/p) = 5 + 10 = 15 and 3 + 5 = 8.  Stream
+    (100, 200, 100) on W = 4: the first iteration takes batches 0 and 2
+    (2 + 2 devices, g = (1, 1), span 15, busy 60, 200 tokens) while batch 1
+    waits; the second runs batch 1 alone (span 8, busy 32, 200 tokens).
+    Filling strictly in stream order would need three iterations (38 ns)."""
+    rows = [(100, 10, 20, 0, 20), (200, 10, 20, 0, 40)]
+    opts = dict(sp_cands=[1, 2, 4], b_max=1, n_heads=4, hidden=0, a2a_alpha_ns=0, g_max=4, mode=D.PLAN_INTRA)
+    (dcp, _), (ref, _) = _both([100, 200, 100], rows, 1, 0, 0, 10, 4, sync=7, **opts)
+    assert dcp == {"iterations": 2, "makespan_ns": 23, "time_ns": 37, "busy_device_ns": 92, "tokens": 400,
+                   "bucket_sp": 0}
+    assert dcp == ref
