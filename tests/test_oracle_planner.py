@@ -13,6 +13,8 @@ import pytest
 
 from oracle import planner as P
 
+import golden_cases
+
 
 def _table(rows, L=4, T_C=5, M_C=10):
     return P.CostTable([P.CostRow(*r) for r in rows], L, T_C, M_C)
@@ -97,6 +99,24 @@ def test_hand_example_accumulation():
 
 COMM_OPTS = dict(sp_cands=(1, 2, 4), n_heads=4, hidden=96, a2a_alpha_ns=100, link_bytes_per_ns=7, g_min=1, g_max=4)
 COMM_TABLE = ((500, 200000, 400000, 0, 500), (1000, 400000, 800000, 0, 1000))
+
+
+@pytest.mark.parametrize("case", golden_cases.planner_cases(), ids=lambda c: c["name"])
+def test_golden_plans(case):
+    """The hand-worked plans above, stored with their citations in
+    tests/golden/planner_hand_examples.json."""
+    t = case["table"]
+    table = _table(t["rows"], L=t["n_layers"], T_C=t["T_C_ns"], M_C=t["M_C_bytes"])
+    o = dict(case["opts"], sp_cands=tuple(case["opts"]["sp_cands"]))
+    out = P.plan(case["seqs"], table, case["budget"], P.PlanOpts(**o), batch_offsets=case["batch_offsets"])
+    for field, want in case["expect"].items():
+        assert getattr(out, field) == want, field
+
+
+def test_golden_accumulation():
+    for c in golden_cases.load("planner_hand_examples.json")["accumulation"]["cases"]:
+        e = c["expect"]
+        assert P.accumulation_steps(c["step_times"], c["g_min"], c["g_max"]) == (e["g"], e["idle"], e["C"])
 
 
 def test_comm_hand_example():

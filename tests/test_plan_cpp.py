@@ -10,6 +10,8 @@ import pytest
 import paper_2608_07524_amd as P
 from oracle import planner as O
 
+import golden_cases
+
 
 def _cpp(seqs, table: O.CostTable, budget, opts: O.PlanOpts, batch_offsets=None):
     kw = dict(sp_cands=tuple(opts.sp_cands), b_max=opts.b_max, n_heads=opts.n_heads, hidden=opts.hidden,
@@ -69,6 +71,18 @@ def test_comm_hand_example():
     assert P.plan([1000], rows, 2, 0, 0, 1500, b_max=1, **dict(kw, sp_cands=(2,))).step_time_ns == [1311328]
     out = P.plan([300, 500], rows, 2, 0, 0, 1500, batch_offsets=[0, 2], b_max=1, **kw)
     assert (out.sp_size, out.step_time_ns) == ([4], [623552])
+
+
+@pytest.mark.parametrize("case", golden_cases.planner_cases(), ids=lambda c: c["name"])
+def test_golden_plans(case):
+    """The C++ planner on the hand-worked plans stored in
+    tests/golden/planner_hand_examples.json."""
+    t = case["table"]
+    o = dict(case["opts"], sp_cands=tuple(case["opts"]["sp_cands"]))
+    out = P.plan(case["seqs"], t["rows"], t["n_layers"], t["T_C_ns"], t["M_C_bytes"], case["budget"],
+                 batch_offsets=case["batch_offsets"], **o)
+    for field, want in case["expect"].items():
+        assert getattr(out, field) == want, field
 
 
 def _ci_table(L=28, h=256):

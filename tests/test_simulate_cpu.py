@@ -137,3 +137,15 @@ def test_window_fill_hand_worked():
     assert dcp == {"iterations": 2, "makespan_ns": 23, "time_ns": 37, "busy_device_ns": 92, "tokens": 400,
                    "bucket_sp": 0}
     assert dcp == ref
+
+
+def test_replay_models_follow_the_paper_table():
+    """The replay's two models carry the layer counts, hidden sizes, head
+    counts and parameter counts of the paper's model-settings table
+    (tests/golden/model_settings.json), with head width hidden / heads."""
+    import golden_cases
+    from paper_2608_07524_amd import replay
+    for name, m in golden_cases.load("model_settings.json")["models"].items():
+        layers, hidden, heads, head_dim, params, _ = replay.MODELS[name]
+        assert (layers, hidden, heads, params) == (m["layers"], m["hidden"], m["heads"], m["params"])
+        assert head_dim * heads == hidden
