@@ -46,9 +46,9 @@ METRIC = "varlen attn fwd+bwd TFLOP/s (valid pairs) + % bf16 MFMA peak, 1 MI355X
 # flops of the whole step (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512).  Valid only
 # for the kernel sources whose hash is recorded with them.
 MEASURED = {
-    "ulysses256k": {"sources_sha256_16": "932de4d4c97aa851", "dkdv_traffic_bytes": 17984391475.6,
+    "ulysses256k": {"sources_sha256_16": "b372c43c8c74253b", "dkdv_traffic_bytes": 17984588870.3,
                     "mfma_flop_per_step": 316663643766784.0},
-    "text": {"sources_sha256_16": "932de4d4c97aa851", "dkdv_traffic_bytes": 14633186520.3,
+    "text": {"sources_sha256_16": "b372c43c8c74253b", "dkdv_traffic_bytes": 14641306222.0,
              "mfma_flop_per_step": 64359992655872.0},
 }
 KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_common.h", "attn_launch.h", "tile_shapes.h")
