@@ -6,8 +6,10 @@
 //   1. bwd_delta:  -Delta = -rowsum(dO o O) and LSE*log2e per (row, head),
 //                  fp32.
 //   2. bwd_dkdv:   key-stationary.  One workgroup per (key tile, head);
-//                  each wavefront keeps the K and V fragments of 32 or 64
-//                  keys and their dK, dV accumulators in registers and walks
+//                  each wavefront keeps the K and V fragments of 32 keys
+//                  (at head width 128 V comes from an LDS copy instead, so
+//                  that two wavefronts fit per SIMD) and their dK, dV
+//                  accumulators in registers and walks
 //                  the query tiles of its own sequence (on or below the
 //                  diagonal when causal), Q / dO tiles streaming through an
 //                  LDS ring:
@@ -226,7 +228,8 @@ __device__ __forceinline__ void to_mfma16_layout(bf16x8& xv, bf16x8& yv) {
 // and a copy of the window's K (both by transposing reads) from LDS.  To
 // fit two workgroups per CU the ring then holds Q and dO once, at the
 // row-read stride, and the transposing reads of dV and dK use that copy.
-template <int D, int KB, int NW, int BM, int NSTAGE, int WPE, bool CAUSAL, bool PACKED, bool FUSED, bool ONECOPY>
+template <int D, int KB, int NW, int BM, int NSTAGE, int WPE, bool CAUSAL, bool PACKED, bool FUSED, bool ONECOPY,
+          bool VLDS>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) void attn_bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
@@ -243,6 +246,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   static_assert(BM % 32 == 0, "whole 32-query blocks per tile");
   static_assert(!FUSED || (PACKED && KB == 1 && BM == 32 && ONECOPY),
                 "fused dQ: packed windows, 32-query tiles, KB 1, one ring copy");
+  static_assert(!VLDS || (KB == 1 && !FUSED && !BwdShape<D>::KV16), "V from LDS: one key block, 32x32 products");
   using DR = DmaTile<BM, RSTR / 8, CPR, NW>;
   using DT = DmaTile<BM, TSTR / 8, CPR, NW>;
   using DL = DmaVecPair<BM, NW>;
@@ -263,6 +267,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   __shared__ __attribute__((aligned(16))) float LV[NSTAGE * 2 * BM];  // LSE*log2e | -Delta
   __shared__ __attribute__((aligned(16))) __bf16 Kt[FUSED ? KTBUF : 8];
   __shared__ __attribute__((aligned(16))) __bf16 dSt[FUSED ? 2 * DSBUF : 8];
+  // (VLDS) the tile's V rows, read 16 bytes per lane as B operands (an odd
+  // number of 16-byte chunks per row: conflict-free); rows past the tile's
+  // keys are zero
+  constexpr int VLSTR = S::DP + 8;
+  using DVL = DmaTile<32 * KB * NW, VLSTR / 8, CPR, NW>;
+  __shared__ __attribute__((aligned(16))) __bf16 Vl[VLDS ? DVL::ELEMS : 8];
   constexpr int NSB = NW * KB;  // 32-key blocks per workgroup
   static_assert(NSB % 2 == 0 && NSTAGE * RBUF >= NSB / 2 * 32 * SSTR, "staging area too small");
   static_assert(NSTAGE >= 2 && NSTAGE <= 4, "ring depth");
@@ -304,10 +314,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
       const int col = 16 * kd + 8 * g;
       if (ok && col < D) {
         kf[kb][kd] = *reinterpret_cast<const bf16x8*>(kh + int64_t(key_t0 + key) * ts + col);
-        vf[kb][kd] = *reinterpret_cast<const bf16x8*>(vh + int64_t(key_t0 + key) * ts + col);
+        if constexpr (!VLDS) vf[kb][kd] = *reinterpret_cast<const bf16x8*>(vh + int64_t(key_t0 + key) * ts + col);
       } else {
         kf[kb][kd] = bf16x8{};
-        vf[kb][kd] = bf16x8{};
+        if constexpr (!VLDS) vf[kb][kd] = bf16x8{};
       }
     }
   }
@@ -315,6 +325,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   // (fused) the window's keys, rows past its end zero; issued before the
   // first ring tile, so the first ring wait covers it
   if constexpr (FUSED) DKT::issue(Kt, kh + int64_t(key_t0) * ts, ts, u.rows, zero, zero, wave, lane);
+  // (VLDS) likewise the tile's V rows
+  if constexpr (VLDS) DVL::issue(Vl, vh + int64_t(key_t0) * ts, ts, u.rows, zero, zero, wave, lane);
 
   const int wave_key_lo = key_t0 + 32 * KB * wave;  // smallest key of this wavefront
   // queries of each key's sequence: [q_lo, q_hi)
@@ -403,6 +415,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   const lds_bf16* Qt3 = ONECOPY ? Qr3 : lds_ptr(Qt);
   const lds_bf16* dOt3 = ONECOPY ? dOr3 : lds_ptr(dOt);
   const lds_f32* LV3 = lds_ptr(LV);
+  const lds_bf16* Vl3 = lds_ptr(Vl);
+  // (VLDS) lane (g, j) reads key 32*(KB*wave + kb) + j, columns 16*kd + 8*g
+  const unsigned vl_off = (32 * KB * wave + j) * VLSTR + 8 * g;
   constexpr unsigned TBUF_R = ONECOPY ? RBUF : TBUF;  // stage size of the transposing-read copies
 
   // (fused) this lane's four 8-byte slots of the dS^T buffer of tile it:
@@ -464,10 +479,53 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
     unsigned rb = st * RBUF + 32 * qb * RSTR + ar_off;
     unsigned tb = st * TBUF_R + 32 * qb * TSTR + tr_off;
     unsigned lb = st * 2 * BM + 32 * qb + 4 * g;
+    unsigned vb = vl_off;
     // Opaque to the optimizer: each read below is then one of these bases
     // plus a constant, which folds into the instruction's offset field
     // (otherwise every read's address is rebuilt with vector arithmetic).
-    asm("" : "+v"(rb), "+v"(tb), "+v"(lb));
+    asm("" : "+v"(rb), "+v"(tb), "+v"(lb), "+v"(vb));
+    if constexpr (VLDS) {
+      // Two wavefronts per SIMD: besides the dK, dV accumulators and the K
+      // fragments only S, dP and the operands of the current 16-column step
+      // stay live (V, Q and dO fragments are read where they are used, LSE
+      // and -Delta per 4-query group).
+      f32x16 sv = f32x16{}, dpv = f32x16{};
+      mfma_prio_hi();
+#pragma unroll
+      for (int kd = 0; kd < NKD; ++kd) {
+        sv = mfma32(lds_read_b128(Qr3 + rb + 16 * kd), kf[0][kd], sv);
+        dpv = mfma32(lds_read_b128(dOr3 + rb + 16 * kd), lds_read_b128(Vl3 + vb + 16 * kd), dpv);
+      }
+      mfma_prio_lo();
+      const int key = wave_key_lo + j;
+      bf16x8 pa2[2], da2[2];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const f32x4 l = lds_read_f32x4(LV3 + lb + 8 * b);
+        const f32x4 n = lds_read_f32x4(LV3 + lb + BM + 8 * b);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int r = 4 * b + c;
+          float p = __builtin_amdgcn_exp2f(fmaf(sv[r], scale_log2, -l[c]));
+          const int qq = qa + 8 * b + 4 * g + c;
+          if (MASK == 1 && key > qq) p = 0.f;
+          if (MASK == 2 && (unsigned(qq - q_lo[0]) >= unsigned(q_hi[0] - q_lo[0]) || (CAUSAL && key > qq))) p = 0.f;
+          pa2[b >> 1][4 * (b & 1) + c] = __bf16(p);
+          da2[b >> 1][4 * (b & 1) + c] = __bf16(p * (dpv[r] + n[c]));
+        }
+      }
+      mfma_prio_hi();
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const unsigned o = tb + 16 * hh * TSTR + 32 * db;
+          dv_acc[0][db] = mfma32(pa2[hh], cat(lds_read_tr(dOt3 + o), lds_read_tr(dOt3 + o + 8 * TSTR)), dv_acc[0][db]);
+          dk_acc[0][db] = mfma32(da2[hh], cat(lds_read_tr(Qt3 + o), lds_read_tr(Qt3 + o + 8 * TSTR)), dk_acc[0][db]);
+        }
+      mfma_prio_lo();
+      return;
+    }
     bf16x8 aq[NKD], ado[NKD];
 #pragma unroll
     for (int kd = 0; kd < NKD; ++kd) {
@@ -492,7 +550,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
       for (int kd = 0; kd < NKD; ++kd) s[kb] = mfma32(aq[kd], kf[kb][kd], s[kb]);
       dp[kb] = nd;
 #pragma unroll
-      for (int kd = 0; kd < NKD; ++kd) dp[kb] = mfma32(ado[kd], vf[kb][kd], dp[kb]);
+      for (int kd = 0; kd < NKD; ++kd)
+        dp[kb] = mfma32(ado[kd], VLDS ? lds_read_b128(Vl3 + vb + 32 * kb * VLSTR + 16 * kd) : vf[kb][kd], dp[kb]);
     }
     mfma_prio_lo();
     f32x4 l4[4];
@@ -597,7 +656,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
         }
         if (MASK == 1) {
           if (qa + 31 < wave_key_lo) continue;  // every query precedes every key
-          if (qa >= wave_key_lo + 32 * KB - 1) {
+          // (V from LDS: one block body per loop keeps the accumulators in
+          // place; the mask costs a compare per element on these few tiles)
+          if (!VLDS && qa >= wave_key_lo + 32 * KB - 1) {
             process_block(st, qb, qa, std::integral_constant<int, 0>{});
             continue;
           }
@@ -955,7 +1016,7 @@ hipError_t launch_dkdv_list(const BwdArgs& a, const WorkUnit* units, int n_units
   constexpr DkdvShape sh = PACKED ? bwd_dkdv_window_shape(D) : bwd_dkdv_shape(D);
   hipLaunchKernelGGL(
       (attn_bwd_dkdv_kernel<D, sh.kb, sh.waves, sh.bm, sh.stages, sh.waves_per_eu, CAUSAL, PACKED, FUSED,
-                            FUSED || sh.onecopy>),
+                            FUSED || sh.onecopy, sh.vlds>),
                      dim3(n_units), dim3(64 * sh.waves), 0, a.stream, static_cast<const __bf16*>(a.q),
                      static_cast<const __bf16*>(a.k), static_cast<const __bf16*>(a.v),
                      static_cast<const __bf16*>(a.dout), a.lse2, a.ndelta, static_cast<__bf16*>(a.dk),

@@ -43,11 +43,12 @@ constexpr int kFwdWaves = 8;
 // Head widths up to 72 run two wavefronts of 32 keys per SIMD, with Q and
 // dO held once per ring stage (the transposing reads of dV and dK use the
 // row-read copy, at the cost of some bank conflicts), which leaves LDS for
-// a four-stage ring of 64-query tiles.  At head width 128 the resident
-// state needs more than the 256 registers two wavefronts per SIMD could
-// each have, so that width runs one wavefront per SIMD; its ring holds Q
-// and dO once too, in two stages of 128-query tiles (139 KB of the 160 KB
-// of LDS), so that a barrier comes every four 32-query blocks.
+// a four-stage ring of 64-query tiles.  At head width 128, K and V
+// fragments plus the dK, dV accumulators would need more than the 256
+// registers two wavefronts per SIMD can each have; V is therefore read from
+// an LDS copy of the tile's 256 V rows (68 KB), which leaves K, the
+// accumulators and one 16-column step of operands in registers (249-256),
+// and the ring holds Q and dO once in two stages of 64-query tiles (76 KB).
 // dQ pass: kBwdDqWaves wavefronts of 32 queries, kBwdDqBN keys per step,
 // K held once per ring stage (its transposing reads share the row-read
 // copy; at head width 128 this also frees the registers the second copy's
@@ -55,9 +56,10 @@ constexpr int kFwdWaves = 8;
 struct DkdvShape {
   int kb, waves, bm, stages, waves_per_eu;
   bool onecopy;  // the ring holds Q and dO once (row-read stride) instead of twice
+  bool vlds;     // V fragments read from an LDS copy of the tile's V rows instead of held in registers
 };
 constexpr DkdvShape bwd_dkdv_shape(int head_dim) {
-  return head_dim > 96 ? DkdvShape{1, 4, 128, 2, 1, true} : DkdvShape{1, 8, 64, 4, 2, true};
+  return head_dim > 96 ? DkdvShape{1, 8, 64, 2, 2, true, true} : DkdvShape{1, 8, 64, 4, 2, true, false};
 }
 constexpr int kBwdDqWaves = 8;
 constexpr int kBwdDqBN = 64;
@@ -79,7 +81,7 @@ constexpr int kWinDkdvBM = 32;
 constexpr DkdvShape bwd_dkdv_window_shape(int head_dim) {
   return head_dim > 96 ? bwd_dkdv_shape(head_dim)
                        : DkdvShape{1, kWinDkdvWaves, kWinDkdvBM, kWinDkdvStages, bwd_dkdv_shape(head_dim).waves_per_eu,
-                                   false};
+                                   false, false};
 }
 // Every query and key of a packed window lies inside the window, so at head
 // widths up to 96 one workgroup computes dQ of its window as well as dK and

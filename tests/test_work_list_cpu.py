@@ -11,12 +11,13 @@ from paper_2608_07524_amd import inputs as I
 
 
 def _tile_rows(pass_, D):
-    return 128 if (pass_ == 1 and D > 96) else 256
+    return 256
 
 
 def _window_rows(pass_, D):
-    """Rows a packed window may span: the window launches' tile."""
-    return 128
+    """Rows a packed window may span: the window launches' tile (the dK/dV
+    pass at head width 128 launches its windows with its tile shape)."""
+    return 256 if (pass_ == 1 and D > 96) else 128
 
 
 def _seq_of_rows(cu):
@@ -102,7 +103,7 @@ def test_tiny_config_and_edges():
     _check(I.tiny().cu_seqlens, 4, 64, False, 0)  # 37 + 64 share one window; 128 and 200 run alone
     _check([0, 0, 0], 2, 72, False, 0)  # only empty sequences
     _check([0, 5], 2, 72, True, 1)  # one short sequence: a plain tile
-    _check([0, 128, 256], 1, 128, False, 1)  # two sequences of exactly one dK/dV tile (D 128)
+    _check([0, 256, 512], 1, 128, False, 1)  # two sequences of exactly one dK/dV tile (D 128)
     _check(np.cumsum([0] + [1] * 600), 1, 72, False, 2)  # 600 one-token sequences
 
 
