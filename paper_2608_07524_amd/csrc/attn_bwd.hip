@@ -488,10 +488,17 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
       // Two wavefronts per SIMD: besides the dK, dV accumulators and the K
       // fragments only S, dP and the operands of the current 16-column step
       // stay live (V, Q and dO fragments are read where they are used, LSE
-      // and -Delta per 4-query group).
+      // per 4-query group).
       // (no issue-priority raise here: with two wavefronts per SIMD it cost
       // about 1 % of the pass)
-      f32x16 sv = f32x16{}, dpv = f32x16{};
+      // the dP accumulator starts at -Delta (the registers dP needs anyway)
+      f32x16 sv = f32x16{}, dpv;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const f32x4 t = lds_read_f32x4(LV3 + lb + BM + 8 * b);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) dpv[4 * b + c] = t[c];
+      }
 #pragma unroll
       for (int kd = 0; kd < NKD; ++kd) {
         sv = mfma32(lds_read_b128(Qr3 + rb + 16 * kd), kf[0][kd], sv);
@@ -502,7 +509,6 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         const f32x4 l = lds_read_f32x4(LV3 + lb + 8 * b);
-        const f32x4 n = lds_read_f32x4(LV3 + lb + BM + 8 * b);
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           const int r = 4 * b + c;
@@ -511,7 +517,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
           if (MASK == 1 && key > qq) p = 0.f;
           if (MASK == 2 && (unsigned(qq - q_lo[0]) >= unsigned(q_hi[0] - q_lo[0]) || (CAUSAL && key > qq))) p = 0.f;
           pa2[b >> 1][4 * (b & 1) + c] = __bf16(p);
-          da2[b >> 1][4 * (b & 1) + c] = __bf16(p * (dpv[r] + n[c]));
+          da2[b >> 1][4 * (b & 1) + c] = __bf16(p * dpv[r]);
         }
       }
       mfma_prio_hi();
