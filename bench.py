@@ -46,9 +46,9 @@ METRIC = "varlen attn fwd+bwd TFLOP/s (valid pairs) + % bf16 MFMA peak, 1 MI355X
 # flops of the whole step (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512).  Valid only
 # for the kernel sources whose hash is recorded with them.
 MEASURED = {
-    "ulysses256k": {"sources_sha256_16": "b372c43c8c74253b", "dkdv_traffic_bytes": 17984588870.3,
+    "ulysses256k": {"sources_sha256_16": "20bbbab6f110d12d", "dkdv_traffic_bytes": 9289883778.6,
                     "mfma_flop_per_step": 316663643766784.0},
-    "text": {"sources_sha256_16": "b372c43c8c74253b", "dkdv_traffic_bytes": 14641306222.0,
+    "text": {"sources_sha256_16": "20bbbab6f110d12d", "dkdv_traffic_bytes": 35629131424.3,
              "mfma_flop_per_step": 64359992655872.0},
 }
 KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_common.h", "attn_launch.h", "tile_shapes.h")

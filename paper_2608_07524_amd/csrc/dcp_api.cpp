@@ -48,23 +48,33 @@ int check_device(int* device) {
 // The constant block at the head of a workspace -- 16-byte chunks the
 // kernels' direct-to-LDS copies read for pad columns ([0 x 8] and
 // [1, 0 x 7] in bf16) and for rows past a sequence end (fp32 +inf) --
-// and each work list with its window masks, copied to their byte offsets
-// in the workspace (one copy per array: the space reserved between them
-// is not touched).
+// and each work list with its window masks at their byte offsets, as one
+// host image and one copy (the space reserved between the lists is
+// zeroed; the per-row areas after the last list are not touched).  One
+// copy instead of one per array: each copy from pageable host memory
+// passes through the runtime's staging buffers, and with many queued
+// behind long kernels the host was seen to wait milliseconds.
 int upload_head(std::initializer_list<ListAt> lists, void* dst, hipStream_t stream) {
-  unsigned char head[kConstBytes];
-  const_head(head);
-  unsigned char* base = static_cast<unsigned char*>(dst);
-  hipError_t e = hipMemcpyAsync(dst, head, sizeof head, hipMemcpyHostToDevice, stream);
+  size_t end = kConstBytes;
   for (const ListAt& l : lists) {
     const UnitList& u = *l.list;
-    if (e == hipSuccess && !u.units.empty())
-      e = hipMemcpyAsync(base + l.units_at, u.units.data(), u.units.size() * sizeof(WorkUnit), hipMemcpyHostToDevice,
-                         stream);
-    if (e == hipSuccess && !u.window_starts.empty())
-      e = hipMemcpyAsync(base + l.windows_at, u.window_starts.data(), u.window_starts.size() * sizeof(uint64_t),
-                         hipMemcpyHostToDevice, stream);
+    if (!u.units.empty()) end = std::max(end, l.units_at + u.units.size() * sizeof(WorkUnit));
+    if (!u.window_starts.empty()) end = std::max(end, l.windows_at + u.window_starts.size() * sizeof(uint64_t));
   }
+  std::vector<unsigned char> img;
+  try {
+    img.assign(end, 0);
+  } catch (const std::bad_alloc&) {
+    return fail(DCP_ERR_INVALID, "out of host memory staging the work lists");
+  }
+  const_head(*reinterpret_cast<unsigned char(*)[kConstBytes]>(img.data()));  // end >= kConstBytes
+  for (const ListAt& l : lists) {
+    const UnitList& u = *l.list;
+    if (!u.units.empty()) std::memcpy(img.data() + l.units_at, u.units.data(), u.units.size() * sizeof(WorkUnit));
+    if (!u.window_starts.empty())
+      std::memcpy(img.data() + l.windows_at, u.window_starts.data(), u.window_starts.size() * sizeof(uint64_t));
+  }
+  const hipError_t e = hipMemcpyAsync(dst, img.data(), end, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
   return DCP_OK;
 }
