@@ -341,6 +341,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   }
   const int q_begin = CAUSAL ? (key_t0 / BM) * BM : 0;
   const int n_qt = (seqlen - q_begin + BM - 1) / BM;
+  // Causal sequence tiles walk their query tiles from the sequence end back
+  // to the diagonal: the key workgroups of one sequence and head, which run
+  // side by side on one die, then read the same Q and dO rows at about the
+  // same time and share them in its L2.  Step it of the walk takes query
+  // tile tile_of(it).
+  constexpr bool REV = CAUSAL && !PACKED;
+  auto tile_of = [&](int it) DCP_INLINE { return REV ? n_qt - 1 - it : it; };
 
   // Full query tiles take the scalar-base copies, except in the causal
   // one-wavefront-per-SIMD variant: its resident state leaves no registers
@@ -350,7 +357,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
   const typename DT::FullOffsets fo_t = DT::full_offsets(ts, wave, lane);
   auto issue_tile = [&](int it) DCP_INLINE {
     const unsigned st = unsigned(it) % NSTAGE;
-    const int q0 = q_begin + it * BM;
+    const int q0 = q_begin + tile_of(it) * BM;
     const int valid = seqlen - q0;
     const __bf16* qs = qh + int64_t(q0) * ts;
     const __bf16* ds = doh + int64_t(q0) * ts;
@@ -638,10 +645,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
     mfma_prio_lo();
   };
 
-  // Query tiles are walked in two phases per wavefront: (causal only) those
-  // reaching its keys, where 32-query blocks entirely before its keys are
-  // skipped and blocks crossing them masked, then those needing no mask.
-  // Every iteration runs the same copy / wait / barrier sequence.
+  // Query tiles are walked in two phases per wavefront: (causal, from the
+  // sequence end) those needing no mask, then those reaching its keys,
+  // where 32-query blocks entirely before its keys are skipped and blocks
+  // crossing them masked.  Every iteration runs the same copy / wait /
+  // barrier sequence.
   // (packed windows: the queries of this wavefront's keys' sequences)
   const int last_key = min(32 * KB - 1, int(u.rows) - 1 - 32 * KB * wave);  // of the wavefront, tile-relative
   const int wq_lo = packed ? (CAUSAL ? wave_key_lo : __builtin_amdgcn_readfirstlane(q_lo[0])) : 0;
@@ -651,7 +659,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
     for (int it = it0; it < it1; ++it) {
       if (it + NSTAGE - 1 < n_qt) issue_tile(it + NSTAGE - 1);
       const unsigned st = unsigned(it) % NSTAGE;
-      const int q0 = q_begin + it * BM;
+      const int q0 = q_begin + tile_of(it) * BM;
       ds_it = it;
 #pragma unroll
       for (int qb = 0; qb < BM / 32; ++qb) {
@@ -699,13 +707,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
       run(it_lo, it_hi, std::integral_constant<int, 2>{});
       idle(it_hi, n_qt);
     } else {
-      int it_plain = 0;
       if (CAUSAL) {
-        // first tile whose queries all follow all of this wavefront's keys
-        it_plain = min(n_qt, max(0, (wave_key_lo + 32 * KB - 1 - q_begin + BM - 1) / BM));
-        run(0, it_plain, std::integral_constant<int, 1>{});
+        // the tiles whose queries all follow all of this wavefront's keys
+        // (from the end), then those crossing or preceding them
+        const int t_plain = min(n_qt, max(0, (wave_key_lo + 32 * KB - 1 - q_begin + BM - 1) / BM));
+        run(0, n_qt - t_plain, std::integral_constant<int, 0>{});
+        run(n_qt - t_plain, n_qt, std::integral_constant<int, 1>{});
+      } else {
+        run(0, n_qt, std::integral_constant<int, 0>{});
       }
-      run(it_plain, n_qt, std::integral_constant<int, 0>{});
     }
   } else {
     idle(0, n_qt);  // no key of the tile (the last tile of a sequence)
