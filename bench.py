@@ -46,9 +46,9 @@ METRIC = "varlen attn fwd+bwd TFLOP/s (valid pairs) + % bf16 MFMA peak, 1 MI355X
 # flops of the whole step (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512).  Valid only
 # for the kernel sources whose hash is recorded with them.
 MEASURED = {
-    "ulysses256k": {"sources_sha256_16": "20bbbab6f110d12d", "dkdv_traffic_bytes": 9289883778.6,
+    "ulysses256k": {"sources_sha256_16": "56ed1303c3c9a4cf", "dkdv_traffic_bytes": 9276192139.0,
                     "mfma_flop_per_step": 316663643766784.0},
-    "text": {"sources_sha256_16": "20bbbab6f110d12d", "dkdv_traffic_bytes": 35629131424.3,
+    "text": {"sources_sha256_16": "56ed1303c3c9a4cf", "dkdv_traffic_bytes": 16167776472.6,
              "mfma_flop_per_step": 64359992655872.0},
 }
 KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_common.h", "attn_launch.h", "tile_shapes.h")
