@@ -201,7 +201,8 @@ void dcp_batch_destroy(dcp_batch batch);
  * padding.  Units [0, *n_tiles) are such sequence tiles (tiles restart at
  * every sequence start, so no block across two sequences is visited).  The
  * rest are packed windows: runs of consecutive sequences, each shorter than
- * the pass's window size (128 rows), sharing one tile of rows
+ * the pass's window size (128 rows; 256 for the dK/dV pass at head width
+ * 128), sharing one tile of rows
  * [row0, row0 + rows) (row0 == seq0), each
  * row attending only within its own sequence; window w = -seqlen - 1 owns
  * window_starts[4w .. 4w+3], where bit x % 64 of word x / 64 is set when a
