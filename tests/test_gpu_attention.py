@@ -82,8 +82,9 @@ def test_tiny_packed_config(torch, causal):
 @pytest.mark.parametrize("D", [64, 72, 128])
 @pytest.mark.parametrize("causal", [False, True])
 def test_ragged_tiles(torch, D, causal):
-    # lengths straddle the 256-row forward tile and the 128/64-row backward tiles
-    lengths = [1, 0, 255, 257, 129, 63, 65, 300, 0, 2]
+    # lengths straddle the 256-row tiles of every pass, the 64-row ring tiles
+    # and the 128-row windows
+    lengths = [1, 0, 255, 257, 129, 63, 65, 300, 0, 2, 513]
     got, ref, n = _run_case(torch, lengths, 3, D, causal, seed=D)
     _assert_close(got, ref, n, f"ragged D={D} causal={causal}")
 
