@@ -528,14 +528,26 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
         }
       }
       mfma_prio_hi();
+      // The transposed operands are read one product ahead: Q's for step n
+      // while dV's product of step n runs, dO's for step n + 1 while dK's
+      // product of step n runs (steps n = (db, hh)).
+      auto operand = [&](const lds_bf16* t3, int n) DCP_INLINE {
+        const unsigned o = tb + 16 * (n & 1) * TSTR + 32 * (n >> 1);
+        return cat(lds_read_tr(t3 + o), lds_read_tr(t3 + o + 8 * TSTR));
+      };
+      // (scheduling fences keep this order: left alone, the compiler issues
+      // each product right behind its own reads and waits on them)
+      bf16x8 bd = operand(dOt3, 0);
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const unsigned o = tb + 16 * hh * TSTR + 32 * db;
-          dv_acc[0][db] = mfma32(pa2[hh], cat(lds_read_tr(dOt3 + o), lds_read_tr(dOt3 + o + 8 * TSTR)), dv_acc[0][db]);
-          dk_acc[0][db] = mfma32(da2[hh], cat(lds_read_tr(Qt3 + o), lds_read_tr(Qt3 + o + 8 * TSTR)), dk_acc[0][db]);
-        }
+      for (int n = 0; n < 2 * NDB; ++n) {
+        const int db = n >> 1, hh = n & 1;
+        const bf16x8 bq = operand(Qt3, n);
+        __builtin_amdgcn_sched_barrier(0);
+        dv_acc[0][db] = mfma32(pa2[hh], bd, dv_acc[0][db]);
+        if (n + 1 < 2 * NDB) bd = operand(dOt3, n + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        dk_acc[0][db] = mfma32(da2[hh], bq, dk_acc[0][db]);
+      }
       mfma_prio_lo();
       return;
     }
