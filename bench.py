@@ -46,9 +46,9 @@ METRIC = "varlen attn fwd+bwd TFLOP/s (valid pairs) + % bf16 MFMA peak, 1 MI355X
 # flops of the whole step (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512).  Valid only
 # for the kernel sources whose hash is recorded with them.
 MEASURED = {
-    "ulysses256k": {"sources_sha256_16": "56ed1303c3c9a4cf", "dkdv_traffic_bytes": 9276192139.0,
+    "ulysses256k": {"sources_sha256_16": "eab350dd7ef8b741", "dkdv_traffic_bytes": 9280745580.9,
                     "mfma_flop_per_step": 316663643766784.0},
-    "text": {"sources_sha256_16": "56ed1303c3c9a4cf", "dkdv_traffic_bytes": 16167776472.6,
+    "text": {"sources_sha256_16": "eab350dd7ef8b741", "dkdv_traffic_bytes": 16185807961.4,
              "mfma_flop_per_step": 64359992655872.0},
 }
 KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_common.h", "attn_launch.h", "tile_shapes.h")
