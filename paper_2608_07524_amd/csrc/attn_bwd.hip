@@ -506,10 +506,22 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE))) 
 #pragma unroll
         for (int c = 0; c < 4; ++c) dpv[4 * b + c] = t[c];
       }
+      // The Q, dO and V fragments of step kd + 1 are read while step kd's
+      // products run (held in that order by scheduling fences).
+      bf16x8 fq[NKD], fo[NKD], fv[NKD];
+      auto fetch = [&](int kd) DCP_INLINE {
+        fq[kd] = lds_read_b128(Qr3 + rb + 16 * kd);
+        fo[kd] = lds_read_b128(dOr3 + rb + 16 * kd);
+        fv[kd] = lds_read_b128(Vl3 + vb + 16 * kd);
+      };
+      fetch(0);
 #pragma unroll
       for (int kd = 0; kd < NKD; ++kd) {
-        sv = mfma32(lds_read_b128(Qr3 + rb + 16 * kd), kf[0][kd], sv);
-        dpv = mfma32(lds_read_b128(dOr3 + rb + 16 * kd), lds_read_b128(Vl3 + vb + 16 * kd), dpv);
+        if (kd + 1 < NKD) fetch(kd + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        sv = mfma32(fq[kd], kf[0][kd], sv);
+        dpv = mfma32(fo[kd], fv[kd], dpv);
+        __builtin_amdgcn_sched_barrier(0);
       }
       const int key = wave_key_lo + j;
       bf16x8 pa2[2], da2[2];
