@@ -921,15 +921,27 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_kernel(
       dp[kb] = FOLD ? nd_init : f32x16{};
     }
     mfma_prio_hi();
-#pragma unroll
-    for (int kd = 0; kd < NKD; ++kd) {
+    // The K and V fragments of step kd + 1 are read while step kd's products
+    // run (held in that order by scheduling fences).
+    bf16x8 fk[NKD][BN / 32], fv[NKD][BN / 32];
+    auto fetch = [&](int kd) DCP_INLINE {
 #pragma unroll
       for (int kb = 0; kb < BN / 32; ++kb) {
-        const bf16x8 ak = lds_read_b128(Ks3 + rb + 32 * kb * KSTR + 16 * kd);
-        s[kb] = mfma32(ak, qf[kd], s[kb]);
-        const bf16x8 av = lds_read_b128(Vs3 + rb + 32 * kb * KSTR + 16 * kd);
-        dp[kb] = mfma32(av, df[kd], dp[kb]);
+        fk[kd][kb] = lds_read_b128(Ks3 + rb + 32 * kb * KSTR + 16 * kd);
+        fv[kd][kb] = lds_read_b128(Vs3 + rb + 32 * kb * KSTR + 16 * kd);
       }
+    };
+    fetch(0);
+#pragma unroll
+    for (int kd = 0; kd < NKD; ++kd) {
+      if (kd + 1 < NKD) fetch(kd + 1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kb = 0; kb < BN / 32; ++kb) {
+        s[kb] = mfma32(fk[kd][kb], qf[kd], s[kb]);
+        dp[kb] = mfma32(fv[kd][kb], df[kd], dp[kb]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
     mfma_prio_lo();
     // Lane (g, j) holds query j against keys k0 + 32kb + 8(r/4) + 4g + r%4.
