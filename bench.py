@@ -46,9 +46,9 @@ METRIC = "varlen attn fwd+bwd TFLOP/s (valid pairs) + % bf16 MFMA peak, 1 MI355X
 # flops of the whole step (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512).  Valid only
 # for the kernel sources whose hash is recorded with them.
 MEASURED = {
-    "ulysses256k": {"sources_sha256_16": "eab350dd7ef8b741", "dkdv_traffic_bytes": 9280745580.9,
+    "ulysses256k": {"sources_sha256_16": "93718f298e98380a", "dkdv_traffic_bytes": 9272405672.1,
                     "mfma_flop_per_step": 316663643766784.0},
-    "text": {"sources_sha256_16": "eab350dd7ef8b741", "dkdv_traffic_bytes": 16185807961.4,
+    "text": {"sources_sha256_16": "93718f298e98380a", "dkdv_traffic_bytes": 16130377848.3,
              "mfma_flop_per_step": 64359992655872.0},
 }
 KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_common.h", "attn_launch.h", "tile_shapes.h")
@@ -390,8 +390,9 @@ def roofline(flop: float, nbytes: float, ms: float, traffic) -> dict:
 
 
 def host_us_per_call(torch, P, w, call, n: int = 5):
-    """Host time of one call, averaged over n enqueued calls (the device is
-    idle at the start and the calls do not wait for it): the per-call API
+    """Host time of one call, averaged over n enqueued calls after one
+    untimed call (the device is idle at the start and the calls do not wait
+    for it): the per-call API
     (dcp_varlen_attn_fwd / _bwd build the work lists on the host and copy
     them to the device each time) against the prepared batch
     (dcp_batch_fwd / _bwd only launch)."""
@@ -417,6 +418,8 @@ def host_us_per_call(torch, P, w, call, n: int = 5):
     }
     out = {}
     for key, fn in runs.items():
+        if fn() != 0:
+            raise RuntimeError(N.last_error())
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(n):

@@ -24,6 +24,11 @@
  * - Ownership: the caller owns every buffer.  The library never allocates
  *   device memory: scratch space comes from a caller-provided workspace whose
  *   size is queried first.  Host arrays are read only during the call.
+ *   dcp_varlen_attn_fwd and dcp_varlen_attn_bwd stage the work lists they
+ *   build in library-owned pinned host memory (per device, four buffers of
+ *   at least 1 MiB, grown by powers of two and kept until the process ends;
+ *   a buffer is reused only after the event behind its last copy, so a host
+ *   more than four calls ahead of the stream waits there).
  * - Streams: `stream` is a hipStream_t passed as void* (NULL = the null
  *   stream).  Attention calls enqueue work and return without synchronising;
  *   argument errors are detected on the host before anything is enqueued;

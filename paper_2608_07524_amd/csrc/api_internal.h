@@ -23,8 +23,10 @@ struct ListAt {
   const UnitList* list;
 };
 // Enqueues on `stream` the copy of the constant chunks to the head of `dst`
-// and of each list to its offsets (the space between them is not touched).
-int upload_head(std::initializer_list<ListAt> lists, void* dst, hipStream_t stream);
+// and of each list to its offsets (the space between them zeroed), from a
+// library-owned pinned staging buffer, or straight from pageable host memory
+// when `pinned` is false (no allocation at all).
+int upload_head(std::initializer_list<ListAt> lists, void* dst, hipStream_t stream, bool pinned = true);
 
 int check_fwd_tensors(const void* q, const void* k, const void* v, const void* o, const float* lse);
 

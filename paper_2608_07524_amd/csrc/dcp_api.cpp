@@ -45,35 +45,129 @@ int check_device(int* device) {
   return DCP_OK;
 }
 
+namespace {
+
+// Pinned host staging for the work-list copies: per device a ring of
+// library-owned pinned buffers, each with an event marking when the copy
+// out of it has run, so that a buffer is rewritten only after its last copy.
+// A copy from pageable memory passes through the runtime's own staging and
+// held the host until the stream had drained the work queued before it
+// (for a backward call behind another, the whole pass); from pinned memory
+// the host only enqueues.  When a list outgrows the ring, every slot moves to
+// new buffers of the next power of two (at least 1 MiB) and the old ones are
+// kept, never freed: freeing pinned memory waits for the device, and a copy
+// may still be reading them.  What is kept stays below the ring's own size.
+// (The no-allocation forward keeps the pageable copy: these are allocations.)
+constexpr int kStageSlots = 4;
+struct StageSlot {
+  unsigned char* host = nullptr;
+  hipEvent_t done = nullptr;
+  bool pending = false;
+};
+struct StageRing {
+  int dev = -1;
+  size_t cap = 0;
+  unsigned next = 0;
+  StageSlot slot[kStageSlots];
+  std::vector<void*> retired;
+};
+std::mutex g_stage_mu;
+std::vector<StageRing*> g_rings;  // one per device, kept until the process ends
+
+int grow_ring(StageRing* r, size_t bytes) {
+  size_t cap = size_t(1) << 20;
+  while (cap < bytes) cap *= 2;
+  for (StageSlot& sl : r->slot) {
+    void* p = nullptr;
+    const hipError_t e = hipHostMalloc(&p, cap, hipHostMallocDefault);
+    if (e != hipSuccess) return fail(DCP_ERR_HIP, "pinned staging of %zu bytes: %s", cap, hipGetErrorString(e));
+    if (sl.host) r->retired.push_back(sl.host);
+    sl.host = static_cast<unsigned char*>(p);
+    sl.pending = false;  // the new buffer has no copy in flight
+  }
+  r->cap = cap;
+  return DCP_OK;
+}
+
 // The constant block at the head of a workspace -- 16-byte chunks the
 // kernels' direct-to-LDS copies read for pad columns ([0 x 8] and
 // [1, 0 x 7] in bf16) and for rows past a sequence end (fp32 +inf) --
-// and each work list with its window masks at their byte offsets, as one
-// host image and one copy (the space reserved between the lists is
-// zeroed; the per-row areas after the last list are not touched).  One
-// copy instead of one per array: each copy from pageable host memory
-// passes through the runtime's staging buffers, and with many queued
-// behind long kernels the host was seen to wait milliseconds.
-int upload_head(std::initializer_list<ListAt> lists, void* dst, hipStream_t stream) {
+// and each work list with its window masks at their byte offsets, written
+// into `img` of `end` bytes (the space reserved between the lists zeroed).
+void fill_image(std::initializer_list<ListAt> lists, unsigned char* img, size_t end) {
+  struct Part {
+    size_t at, bytes;
+    const void* src;
+  };
+  std::vector<Part> parts;
+  parts.reserve(2 * lists.size());
+  for (const ListAt& l : lists) {
+    const UnitList& u = *l.list;
+    if (!u.units.empty()) parts.push_back({l.units_at, u.units.size() * sizeof(WorkUnit), u.units.data()});
+    if (!u.window_starts.empty())
+      parts.push_back({l.windows_at, u.window_starts.size() * sizeof(uint64_t), u.window_starts.data()});
+  }
+  std::sort(parts.begin(), parts.end(), [](const Part& a, const Part& b) { return a.at < b.at; });
+  const_head(*reinterpret_cast<unsigned char(*)[kConstBytes]>(img));  // end >= kConstBytes
+  size_t at = kConstBytes;
+  for (const Part& p : parts) {  // the parts do not overlap and end by `end`
+    std::memset(img + at, 0, p.at - at);
+    std::memcpy(img + p.at, p.src, p.bytes);
+    at = p.at + p.bytes;
+  }
+  std::memset(img + at, 0, end - at);
+}
+
+int upload_pinned(std::initializer_list<ListAt> lists, size_t end, void* dst, hipStream_t stream) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  std::lock_guard<std::mutex> lock(g_stage_mu);
+  StageRing* ring = nullptr;
+  for (StageRing* r : g_rings)
+    if (r->dev == dev) ring = r;
+  if (!ring) {
+    ring = new (std::nothrow) StageRing{};
+    if (!ring) return fail(DCP_ERR_INVALID, "out of host memory");
+    ring->dev = dev;
+    g_rings.push_back(ring);
+  }
+  int st;
+  if (ring->cap < end && (st = grow_ring(ring, end))) return st;
+  StageSlot& sl = ring->slot[ring->next++ % kStageSlots];
+  if (sl.pending && (e = hipEventSynchronize(sl.done)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "work list staging: %s", hipGetErrorString(e));
+  sl.pending = false;
+  if (!sl.done && (e = hipEventCreateWithFlags(&sl.done, hipEventDisableTiming)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "staging event: %s", hipGetErrorString(e));
+  fill_image(lists, sl.host, end);
+  if ((e = hipMemcpyAsync(dst, sl.host, end, hipMemcpyHostToDevice, stream)) != hipSuccess ||
+      (e = hipEventRecord(sl.done, stream)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
+  sl.pending = true;
+  return DCP_OK;
+}
+
+}  // namespace
+
+// The lists as one host image and one copy, through the pinned staging ring
+// unless `pinned` is false (the per-row areas after the last list are not
+// touched).
+int upload_head(std::initializer_list<ListAt> lists, void* dst, hipStream_t stream, bool pinned) {
   size_t end = kConstBytes;
   for (const ListAt& l : lists) {
     const UnitList& u = *l.list;
     if (!u.units.empty()) end = std::max(end, l.units_at + u.units.size() * sizeof(WorkUnit));
     if (!u.window_starts.empty()) end = std::max(end, l.windows_at + u.window_starts.size() * sizeof(uint64_t));
   }
+  if (pinned) return upload_pinned(lists, end, dst, stream);
   std::vector<unsigned char> img;
   try {
-    img.assign(end, 0);
+    img.resize(end);
   } catch (const std::bad_alloc&) {
     return fail(DCP_ERR_INVALID, "out of host memory staging the work lists");
   }
-  const_head(*reinterpret_cast<unsigned char(*)[kConstBytes]>(img.data()));  // end >= kConstBytes
-  for (const ListAt& l : lists) {
-    const UnitList& u = *l.list;
-    if (!u.units.empty()) std::memcpy(img.data() + l.units_at, u.units.data(), u.units.size() * sizeof(WorkUnit));
-    if (!u.window_starts.empty())
-      std::memcpy(img.data() + l.windows_at, u.window_starts.data(), u.window_starts.size() * sizeof(uint64_t));
-  }
+  fill_image(lists, img.data(), end);
   const hipError_t e = hipMemcpyAsync(dst, img.data(), end, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
   return DCP_OK;

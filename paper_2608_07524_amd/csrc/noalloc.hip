@@ -75,6 +75,6 @@ extern "C" int dcp_varlen_attn_fwd_noalloc(const dcp_attn_desc* desc, const void
   void* ws = nullptr;
   if ((st = scratch_ptr(dev, &ws))) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = upload_head({{units_at, windows_at, &units}}, ws, s))) return st;
+  if ((st = upload_head({{units_at, windows_at, &units}}, ws, s, /*pinned=*/false))) return st;
   return run_fwd(desc, units, q, k, v, o, lse, static_cast<char*>(ws), units_at, windows_at, s);
 }

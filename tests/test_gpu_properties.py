@@ -77,6 +77,42 @@ def test_prepared_batch_equals_per_call(torch, D, causal, lengths):
             assert np.array_equal(x, y)
 
 
+def test_per_call_queue_deeper_than_staging_ring(torch):
+    """The per-call entry points stage their lists in a ring of four pinned
+    host buffers per device: ten calls enqueued with no synchronisation
+    (the ring wraps), with a backward whose lists pass 1 MiB halfway (the
+    ring grows while earlier copies may still be in flight), give the
+    prepared batch's results bit for bit."""
+    import paper_2608_07524_amd as P
+    torch.manual_seed(5)
+    cases = {"small": ([700, 1, 2049, 300], 4, 128), "large": ([1024] * 128, 64, 64)}
+    data, ref = {}, {}
+    for name, (lengths, H, D) in cases.items():
+        cu = I.cu_from_lengths(lengths)
+        T = int(cu[-1])
+        q, k, v, do = (torch.randn(T, H, D, device="cuda").to(torch.bfloat16) for _ in range(4))
+        call = P.PreparedAttention(q, k, v, do, cu, 1 / math.sqrt(D), True)
+        call.step()
+        torch.cuda.synchronize()
+        data[name] = (cu, q, k, v, do, D)
+        ref[name] = [t.clone() for t in (call.o, call.lse, call.dq, call.dk, call.dv)]
+        del call
+    torch.cuda.synchronize()
+    got = []
+    for name in ["small"] * 3 + ["large"] + ["small"] * 2:
+        cu, q, k, v, do, D = data[name]
+        o, lse = P.varlen_attn_fwd(q, k, v, cu, 1 / math.sqrt(D), True)
+        if name == "large" or len(got) < 4:
+            dq, dk, dv = P.varlen_attn_bwd(do, o, lse, q, k, v, cu, 1 / math.sqrt(D), True)
+            got.append((name, [o, lse, dq, dk, dv]))
+        else:
+            got.append((name, [o, lse]))
+    torch.cuda.synchronize()
+    for name, outs in got:
+        for x, y in zip(outs, ref[name]):
+            assert torch.equal(x, y), name
+
+
 @pytest.mark.parametrize("causal", [False, True])
 def test_position_in_pack_invariance(torch, causal):
     """A sequence's outputs do not depend on where it sits in the pack or
