@@ -24,7 +24,14 @@
 // accumulators stay far from fp32 limits; the result O = acc / l does not
 // depend on which m was used.  When the head width leaves a spare padded
 // row in the last 32-row block of O^T (D = 72), a column of ones appended to
-// V makes the matrix cores produce the row sum l = sum_j P_ij as well.
+// V makes the matrix cores produce the row sum l = sum_j P_ij as well, and
+// each block's row max decides the move.  Otherwise (D = 64, 128) the row
+// sum is formed on the vector ALUs anyway, and it replaces the row max: a
+// lane's 16 weights of a block sum to at most 2^8 unless one of them may
+// exceed 2^8, so only a block whose sum passes 2^8 (rarely; in a packed
+// window also a row's first block with keys of its own, where the weights
+// against the initial m overflow) takes its row max, moves m and forms its
+// weights again.
 // Epilogue: O = O^T / l (bf16), LSE = (m + log2 l) * ln 2.
 #include <type_traits>
 
@@ -40,6 +47,7 @@ constexpr int kFwdStages = 4;
 static_assert(kFwdStages >= 3 && kWinFwdStages >= 3, "tiles kt and kt + 1 are read while kt + 2 lands");
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 constexpr float kNoMax = -1e30f;       // running max before any key
+constexpr float kSumBound = 256.0f;    // 2^kRescaleSlack
 
 template <int D>
 struct FwdShape {
@@ -281,6 +289,17 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
     }
   };
 
+  // Unconditional move of m to the larger of m and mx (a wave-uniform
+  // branch has already been taken).
+  auto move_max = [&](float mx) DCP_INLINE {
+    const float m_new = fmaxf(m_use, mx);
+    const float alpha = __builtin_amdgcn_exp2f(m_use - m_new);
+    m_use = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
+  };
+
   // O^T += V^T P^T for the current block (V rows at vcur, this lane's
   // transposing-read offset included).  32x32 blocks: A = V^T rows
   // 32db + (lane % 32) over keys 16hh + 4g + {0..3, 8..11}, B = pb[hh]
@@ -346,8 +365,8 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
 
   // One pipelined step: P and O for the current block (V rows at vcur)
   // while the scores of block bn (K fragments already in kn) are computed,
-  // masked when MASK, and their row max taken; kn then receives the K
-  // fragments of block bn + 1 (K rows at kafter).  On a wavefront's last
+  // masked when MASK, and (D = 72) their row max taken; kn then receives
+  // the K fragments of block bn + 1 (K rows at kafter).  On a wavefront's last
   // block the successor's scores are computed but not used (valid_next
   // false), and the reads ahead stay inside the ring.
   auto step = [&](int bn, unsigned kafter, unsigned vcur, bool valid_next, auto mask_tag) DCP_INLINE {
@@ -355,28 +374,43 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_kernel(const __bf16* __restr
     f32x16 sn = scores(kn);
     load_k(kafter, kn);
     // P = exp2(S*scale*log2e - m) as bf16 (B operand of the PV product)
-    const float mneg = -m_use;
     bf16x8 pb[2];
+    auto exps = [&]() DCP_INLINE {
+      const float mneg = -m_use;
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
+      for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pb[hh][e] = __bf16(__builtin_amdgcn_exp2f(fmaf(sc[8 * hh + e], scale_log2, mneg)));
+        for (int e = 0; e < 8; ++e) pb[hh][e] = __bf16(__builtin_amdgcn_exp2f(fmaf(sc[8 * hh + e], scale_log2, mneg)));
+    };
+    exps();
     if constexpr (!S::ONES_ROW) {
       // the row sum over the same bf16 weights the PV product uses, so that
       // O = sum_j w_j v_j / sum_j w_j is an exact weighted mean of V rows
       // (pairwise dot products with (1, 1), one accumulator per half)
-      const bf16x2 one = {__bf16(1.f), __bf16(1.f)};
-      float lh[2] = {0.f, 0.f};
+      auto psum = [&]() DCP_INLINE {
+        const bf16x2 one = {__bf16(1.f), __bf16(1.f)};
+        float lh[2] = {0.f, 0.f};
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
+        for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          lh[hh] = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[hh][2 * i], pb[hh][2 * i + 1]}, one, lh[hh], false);
-      l_run += lh[0] + lh[1];
+          for (int i = 0; i < 4; ++i)
+            lh[hh] = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[hh][2 * i], pb[hh][2 * i + 1]}, one, lh[hh], false);
+        return lh[0] + lh[1];
+      };
+      // The lane's 16 weights sum to at most 2^8 unless one of them may
+      // exceed 2^8 (or overflowed): only then is the block's row max taken,
+      // m moved to it and the weights formed again (at most 1 each).
+      float ls = psum();
+      if (__builtin_amdgcn_ballot_w64(!(ls <= kSumBound))) {
+        move_max(row_max(sc));
+        exps();
+        ls = psum();
+      }
+      l_run += ls;
     }
     if constexpr (MASK) apply_mask(sn, bn);
     pv_product(pb, vcur);
-    rescale(row_max(sn), valid_next);
+    if constexpr (S::ONES_ROW) rescale(row_max(sn), valid_next);
     sc = sn;
   };
 

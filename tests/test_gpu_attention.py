@@ -31,13 +31,15 @@ def torch():
     return t
 
 
-def _run_case(torch, lengths, H, D, causal, scale=None, seed=0):
+def _run_case(torch, lengths, H, D, causal, scale=None, seed=0, key_gain=None):
     import paper_2608_07524_amd as P
     rng = np.random.default_rng(seed)
     cu = I.cu_from_lengths(lengths)
     n = int(cu[-1])
     T = n + GUARD
     bits = I.tensors(rng, T, H, D)
+    if key_gain is not None:  # per-row factors on K (length T)
+        bits[1] = I.bf16_bits(I.bf16_to_f64(bits[1]) * np.asarray(key_gain, dtype=np.float64)[:, None, None])
     scale = 1.0 / math.sqrt(D) if scale is None else scale
     q, k, v, do = (to_device(torch, b) for b in bits)
     sentinel = torch.full((T, H, D), 7.0, dtype=torch.bfloat16, device="cuda")
@@ -113,3 +115,26 @@ def test_packed_windows(torch, D, causal):
 def test_single_long_sequence(torch):
     got, ref, n = _run_case(torch, [1500], 2, 128, False, seed=9)
     _assert_close(got, ref, n, "one 1500-token sequence")
+
+
+@pytest.mark.parametrize("D", [64, 72, 128])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("regime", ["key_ramp", "sharp"])
+def test_running_max_moves(torch, D, causal, regime):
+    """Scores whose row maxima keep rising along the keys, so that the
+    online softmax's running max moves many times by more than its lazy
+    slack (2^8 in the exponent) inside one row: K rows scaled from 0.25 to
+    6.25 along each sequence, or scale 1 instead of 1/sqrt(D) (nearly
+    one-hot rows)."""
+    lengths = [1100, 37, 600, 0, 257]
+    cu = I.cu_from_lengths(lengths)
+    gain = np.ones(int(cu[-1]) + GUARD)
+    scale = None
+    if regime == "key_ramp":
+        for b in range(len(lengths)):
+            s0, s1 = int(cu[b]), int(cu[b + 1])
+            gain[s0:s1] = 0.25 + 6.0 * np.arange(s1 - s0) / max(1, s1 - s0 - 1)
+    else:
+        scale = 1.0
+    got, ref, n = _run_case(torch, lengths, 2, D, causal, scale, seed=60 + D, key_gain=gain)
+    _assert_close(got, ref, n, f"running max {regime} D={D} causal={causal}")
