@@ -46,9 +46,9 @@ METRIC = "varlen attn fwd+bwd TFLOP/s (valid pairs) + % bf16 MFMA peak, 1 MI355X
 # flops of the whole step (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512).  Valid only
 # for the kernel sources whose hash is recorded with them.
 MEASURED = {
-    "ulysses256k": {"sources_sha256_16": "93718f298e98380a", "dkdv_traffic_bytes": 9272405672.1,
+    "ulysses256k": {"sources_sha256_16": "80d2e41c985b0cf9", "dkdv_traffic_bytes": 9277695477.7,
                     "mfma_flop_per_step": 316663643766784.0},
-    "text": {"sources_sha256_16": "93718f298e98380a", "dkdv_traffic_bytes": 16130377848.3,
+    "text": {"sources_sha256_16": "80d2e41c985b0cf9", "dkdv_traffic_bytes": 16165009969.4,
              "mfma_flop_per_step": 64359992655872.0},
 }
 KERNEL_SOURCES = ("attn_fwd.hip", "attn_bwd.hip", "attn_common.h", "attn_launch.h", "tile_shapes.h")
