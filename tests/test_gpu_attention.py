@@ -138,3 +138,28 @@ def test_running_max_moves(torch, D, causal, regime):
         scale = 1.0
     got, ref, n = _run_case(torch, lengths, 2, D, causal, scale, seed=60 + D, key_gain=gain)
     _assert_close(got, ref, n, f"running max {regime} D={D} causal={causal}")
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_only_empty_sequences(torch, causal):
+    """A batch whose sequences are all empty: every call returns without
+    touching an output row (per call and through a prepared batch)."""
+    import paper_2608_07524_amd as P
+    cu = I.cu_from_lengths([0, 0, 0])
+    T, H, D = GUARD, 2, 128
+    bits = I.tensors(np.random.default_rng(1), T, H, D)
+    q, k, v, do = (to_device(torch, b) for b in bits)
+    sentinel = torch.full((T, H, D), 7.0, dtype=torch.bfloat16, device="cuda")
+    o, dq, dk, dv = (sentinel.clone() for _ in range(4))
+    lse = torch.full((H, T), 7.0, dtype=torch.float32, device="cuda")
+    P.varlen_attn_fwd(q, k, v, cu, None, causal, out=o, lse=lse)
+    P.varlen_attn_bwd(do, o, lse, q, k, v, cu, None, causal, dq=dq, dk=dk, dv=dv)
+    call = P.PreparedAttention(q, k, v, do, cu, None, causal)
+    for t in (call.o, call.dq, call.dk, call.dv):
+        t.fill_(7.0)
+    call.lse.fill_(7.0)
+    call.step()
+    torch.cuda.synchronize()
+    for t in (o, dq, dk, dv, call.o, call.dq, call.dk, call.dv):
+        assert bool((t == 7.0).all())
+    assert bool((lse == 7.0).all()) and bool((call.lse == 7.0).all())
