@@ -91,6 +91,15 @@ def test_ragged_tiles(torch, D, causal):
     _assert_close(got, ref, n, f"ragged D={D} causal={causal}")
 
 
+@pytest.mark.parametrize("H,D,causal", [(1, 128, False), (1, 72, True), (64, 64, True), (48, 128, False)])
+def test_head_counts(torch, H, D, causal):
+    """One head, and many heads (head index above any small-count fast path;
+    tiles of all heads interleaved in the per-die lists)."""
+    lengths = [300, 1, 129, 64, 0, 257]
+    got, ref, n = _run_case(torch, lengths, H, D, causal, seed=70 + H + D)
+    _assert_close(got, ref, n, f"H={H} D={D} causal={causal}")
+
+
 def test_many_tiny_sequences(torch):
     rng = np.random.default_rng(5)
     lengths = rng.integers(1, 17, 300).tolist()
