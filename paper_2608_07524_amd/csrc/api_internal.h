@@ -16,16 +16,10 @@ namespace dcp {
 // null), else DCP_ERR_HIP with the thread's error message set.
 int check_device(int* device = nullptr);
 
-// One work list with its window masks, to be copied to byte offsets
-// units_at / windows_at of a device buffer.
-struct ListAt {
-  size_t units_at, windows_at;
-  const UnitList* list;
-};
-// Enqueues on `stream` the copy of the constant chunks to the head of `dst`
-// and of each list to its offsets (the space between them zeroed), from a
+// Enqueues on `stream` the copies of the constant chunks to the head of
+// `dst` and of each list to its offsets (plan_upload's segments), from a
 // library-owned pinned staging buffer, or straight from pageable host memory
-// when `pinned` is false (no allocation at all).
+// when `pinned` is false (no allocation on the device or of pinned memory).
 int upload_head(std::initializer_list<ListAt> lists, void* dst, hipStream_t stream, bool pinned = true);
 
 int check_fwd_tensors(const void* q, const void* k, const void* v, const void* o, const float* lse);

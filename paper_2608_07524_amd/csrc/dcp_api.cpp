@@ -89,36 +89,19 @@ int grow_ring(StageRing* r, size_t bytes) {
   return DCP_OK;
 }
 
-// The constant block at the head of a workspace -- 16-byte chunks the
-// kernels' direct-to-LDS copies read for pad columns ([0 x 8] and
-// [1, 0 x 7] in bf16) and for rows past a sequence end (fp32 +inf) --
-// and each work list with its window masks at their byte offsets, written
-// into `img` of `end` bytes (the space reserved between the lists zeroed).
-void fill_image(std::initializer_list<ListAt> lists, unsigned char* img, size_t end) {
-  struct Part {
-    size_t at, bytes;
-    const void* src;
-  };
-  std::vector<Part> parts;
-  parts.reserve(2 * lists.size());
-  for (const ListAt& l : lists) {
-    const UnitList& u = *l.list;
-    if (!u.units.empty()) parts.push_back({l.units_at, u.units.size() * sizeof(WorkUnit), u.units.data()});
-    if (!u.window_starts.empty())
-      parts.push_back({l.windows_at, u.window_starts.size() * sizeof(uint64_t), u.window_starts.data()});
+// One copy per segment, from the host buffer fill_segments wrote.
+int copy_segments(const UploadPlan& u, const unsigned char* buf, void* dst, hipStream_t stream) {
+  size_t off = 0;
+  for (const UploadSegment& g : u.segs) {
+    const hipError_t e =
+        hipMemcpyAsync(static_cast<char*>(dst) + g.at, buf + off, g.end - g.at, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
+    off += g.end - g.at;
   }
-  std::sort(parts.begin(), parts.end(), [](const Part& a, const Part& b) { return a.at < b.at; });
-  const_head(*reinterpret_cast<unsigned char(*)[kConstBytes]>(img));  // end >= kConstBytes
-  size_t at = kConstBytes;
-  for (const Part& p : parts) {  // the parts do not overlap and end by `end`
-    std::memset(img + at, 0, p.at - at);
-    std::memcpy(img + p.at, p.src, p.bytes);
-    at = p.at + p.bytes;
-  }
-  std::memset(img + at, 0, end - at);
+  return DCP_OK;
 }
 
-int upload_pinned(std::initializer_list<ListAt> lists, size_t end, void* dst, hipStream_t stream) {
+int upload_pinned(const UploadPlan& u, void* dst, hipStream_t stream) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(DCP_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
@@ -133,44 +116,38 @@ int upload_pinned(std::initializer_list<ListAt> lists, size_t end, void* dst, hi
     g_rings.push_back(ring);
   }
   int st;
-  if (ring->cap < end && (st = grow_ring(ring, end))) return st;
+  if (ring->cap < u.bytes && (st = grow_ring(ring, u.bytes))) return st;
   StageSlot& sl = ring->slot[ring->next++ % kStageSlots];
   if (sl.pending && (e = hipEventSynchronize(sl.done)) != hipSuccess)
     return fail(DCP_ERR_HIP, "work list staging: %s", hipGetErrorString(e));
   sl.pending = false;
   if (!sl.done && (e = hipEventCreateWithFlags(&sl.done, hipEventDisableTiming)) != hipSuccess)
     return fail(DCP_ERR_HIP, "staging event: %s", hipGetErrorString(e));
-  fill_image(lists, sl.host, end);
-  if ((e = hipMemcpyAsync(dst, sl.host, end, hipMemcpyHostToDevice, stream)) != hipSuccess ||
-      (e = hipEventRecord(sl.done, stream)) != hipSuccess)
-    return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
+  fill_segments(u, sl.host);
+  if ((st = copy_segments(u, sl.host, dst, stream))) return st;
+  if ((e = hipEventRecord(sl.done, stream)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "work list staging: %s", hipGetErrorString(e));
   sl.pending = true;
   return DCP_OK;
 }
 
 }  // namespace
 
-// The lists as one host image and one copy, through the pinned staging ring
-// unless `pinned` is false (the per-row areas after the last list are not
-// touched).
+// The constant chunks and the lists as plan_upload's segments, through the
+// pinned staging ring unless `pinned` is false (the per-row areas after the
+// last list, and the space reserved between segments, are not touched).
 int upload_head(std::initializer_list<ListAt> lists, void* dst, hipStream_t stream, bool pinned) {
-  size_t end = kConstBytes;
-  for (const ListAt& l : lists) {
-    const UnitList& u = *l.list;
-    if (!u.units.empty()) end = std::max(end, l.units_at + u.units.size() * sizeof(WorkUnit));
-    if (!u.window_starts.empty()) end = std::max(end, l.windows_at + u.window_starts.size() * sizeof(uint64_t));
-  }
-  if (pinned) return upload_pinned(lists, end, dst, stream);
+  UploadPlan u;
   std::vector<unsigned char> img;
   try {
-    img.resize(end);
+    u = plan_upload(lists.begin(), lists.size());
+    if (!pinned) img.resize(u.bytes);
   } catch (const std::bad_alloc&) {
     return fail(DCP_ERR_INVALID, "out of host memory staging the work lists");
   }
-  fill_image(lists, img.data(), end);
-  const hipError_t e = hipMemcpyAsync(dst, img.data(), end, hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return fail(DCP_ERR_HIP, "work list upload: %s", hipGetErrorString(e));
-  return DCP_OK;
+  if (pinned) return upload_pinned(u, dst, stream);
+  fill_segments(u, img.data());
+  return copy_segments(u, img.data(), dst, stream);
 }
 
 int check_fwd_tensors(const void* q, const void* k, const void* v, const void* o, const float* lse) {

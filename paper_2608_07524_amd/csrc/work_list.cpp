@@ -225,6 +225,46 @@ BwdLayout bwd_layout(const dcp_attn_desc* d) {
   return l;
 }
 
+UploadPlan plan_upload(const ListAt* lists, size_t n_lists) {
+  UploadPlan u;
+  u.parts.reserve(1 + 2 * n_lists);
+  u.parts.push_back({0, kConstBytes, nullptr});
+  for (size_t i = 0; i < n_lists; ++i) {
+    const UnitList& x = *lists[i].list;
+    if (!x.units.empty()) u.parts.push_back({lists[i].units_at, x.units.size() * sizeof(WorkUnit), x.units.data()});
+    if (!x.window_starts.empty())
+      u.parts.push_back({lists[i].windows_at, x.window_starts.size() * sizeof(uint64_t), x.window_starts.data()});
+  }
+  std::sort(u.parts.begin(), u.parts.end(), [](const UploadPart& p, const UploadPart& q) { return p.at < q.at; });
+  for (const UploadPart& p : u.parts) {  // the parts do not overlap
+    if (!u.segs.empty() && p.at - u.segs.back().end <= kMergeGap)
+      u.segs.back().end = p.at + p.bytes;
+    else
+      u.segs.push_back({p.at, p.at + p.bytes});
+  }
+  for (const UploadSegment& g : u.segs) u.bytes += g.end - g.at;
+  return u;
+}
+
+void fill_segments(const UploadPlan& u, unsigned char* buf) {
+  size_t off = 0;  // host offset of the current segment
+  size_t k = 0;    // next part
+  for (const UploadSegment& g : u.segs) {
+    size_t at = g.at;
+    for (; k < u.parts.size() && u.parts[k].at < g.end; ++k) {
+      const UploadPart& p = u.parts[k];
+      unsigned char* out = buf + off + (p.at - g.at);
+      std::memset(buf + off + (at - g.at), 0, p.at - at);
+      if (p.src)
+        std::memcpy(out, p.src, p.bytes);
+      else
+        const_head(*reinterpret_cast<unsigned char(*)[kConstBytes]>(out));
+      at = p.at + p.bytes;
+    }
+    off += g.end - g.at;
+  }
+}
+
 int batch_init(const dcp_attn_desc* desc, dcp_batch_s* b) {
   int st = validate_desc(desc);
   if (st) return st;

@@ -55,6 +55,36 @@ struct BwdLayout {
 };
 BwdLayout bwd_layout(const dcp_attn_desc* d);
 
+// One work list with its window masks, to be copied to byte offsets
+// units_at / windows_at of a device buffer.
+struct ListAt {
+  size_t units_at, windows_at;
+  const UnitList* list;
+};
+// What an upload writes: the constant chunks at offset 0 and each list and
+// its window masks at their offsets.  A per-call workspace reserves room for
+// the longest possible list ahead of the next one, so these parts can lie
+// megabytes apart: parts at most kMergeGap apart form one segment (the bytes
+// between them zeroed), the others segments of their own, which a host
+// buffer holds back to back; the space between segments is neither filled
+// nor copied.
+constexpr size_t kMergeGap = size_t(16) << 10;
+struct UploadPart {
+  size_t at, bytes;
+  const void* src;  // null: the constant chunks
+};
+struct UploadSegment {
+  size_t at, end;  // device byte range
+};
+struct UploadPlan {
+  std::vector<UploadPart> parts;  // by offset
+  std::vector<UploadSegment> segs;
+  size_t bytes = 0;  // host bytes: the segments back to back
+};
+UploadPlan plan_upload(const ListAt* lists, size_t n_lists);
+// Writes the segments back to back into `buf` (plan.bytes bytes).
+void fill_segments(const UploadPlan& plan, unsigned char* buf);
+
 }  // namespace dcp
 
 // A prepared batch (dcp_batch in dcp.h): a copy of the descriptor and of

@@ -14,8 +14,11 @@
 //   S <same as P> n_devices bucket_sp iter_sync_ns
 //   W n_seqs cu.. total_tokens n_heads head_dim causal scale_milli pass
 //   B n_seqs cu.. total_tokens n_heads head_dim causal scale_milli
+//   U n_seqs cu.. total_tokens n_heads head_dim causal scale_milli kind
+//     (kind 0: per-call forward workspace, 1: per-call backward, 2: prepared batch)
 #include <cstdio>
 #include <cstdlib>
+#include <cstring>
 #include <vector>
 
 #include "dcp.h"
@@ -178,6 +181,71 @@ void run_batch() {
   std::printf("\n");
 }
 
+// The work-list upload as the device would receive it: plan_upload's
+// segments filled on the host and copied into an image of the list area
+// (pre-filled with 0xAB); then every part must sit at its offset, the bytes
+// between the parts of a segment must be zero and everything outside the
+// segments must be untouched.
+void run_upload() {
+  dcp_attn_desc d{};
+  std::vector<int32_t> cu;
+  read_desc(d, cu);
+  const int kind = int(need());
+  const int s = dcp::validate_desc(&d);
+  std::printf("%d", s);
+  if (s != DCP_OK) {
+    std::printf("\n");
+    return;
+  }
+  dcp::UnitList l0, l1;
+  dcp_batch_s b;
+  std::vector<dcp::ListAt> lists;
+  size_t area = 0;
+  if (kind == 0) {
+    const dcp::FwdLayout f = dcp::fwd_layout(&d);
+    l0 = dcp::build_pass(&d, dcp::kPassFwd);
+    lists = {{f.units, f.windows, &l0}};
+    area = f.total;
+  } else if (kind == 1) {
+    const dcp::BwdLayout bl = dcp::bwd_layout(&d);
+    l0 = dcp::build_pass(&d, dcp::kPassDkdv);
+    l1 = dcp::build_pass(&d, dcp::kPassDq);
+    lists = {{bl.units, bl.windows, &l0}, {bl.qunits, bl.qwindows, &l1}};
+    area = bl.lse2;
+  } else {
+    if (dcp::batch_init(&d, &b) != DCP_OK) std::exit(3);
+    for (int p = 0; p < 3; ++p) lists.push_back({b.units_at[p], b.windows_at[p], &b.pass[p]});
+    area = b.lse2_at;
+  }
+  const dcp::UploadPlan u = dcp::plan_upload(lists.data(), lists.size());
+  std::vector<unsigned char> buf(u.bytes), img(area, 0xAB), inside(area, 0);
+  dcp::fill_segments(u, buf.data());
+  size_t off = 0;
+  bool ok = true;
+  for (const dcp::UploadSegment& g : u.segs) {
+    ok = ok && g.end <= area && g.at < g.end;
+    if (!ok) break;
+    std::memcpy(img.data() + g.at, buf.data() + off, g.end - g.at);
+    std::memset(inside.data() + g.at, 1, g.end - g.at);
+    off += g.end - g.at;
+  }
+  ok = ok && off == u.bytes;
+  if (ok) {
+    unsigned char head[dcp::kConstBytes];
+    dcp::const_head(head);
+    ok = std::memcmp(img.data(), head, dcp::kConstBytes) == 0;
+    for (const dcp::UploadPart& p : u.parts) {
+      if (p.src) ok = ok && std::memcmp(img.data() + p.at, p.src, p.bytes) == 0;
+      std::memset(inside.data() + p.at, 2, p.bytes);
+    }
+    for (size_t i = 0; i < area && ok; ++i)
+      ok = inside[i] == 2 || (inside[i] == 1 ? img[i] == 0 : img[i] == 0xAB);
+  }
+  size_t part_bytes = 0;
+  for (const dcp::UploadPart& p : u.parts) part_bytes += p.bytes;
+  std::printf(" %d %zu %zu %zu %zu\n", int(ok), u.segs.size(), u.bytes, part_bytes, area);
+}
+
 }  // namespace
 
 int main() {
@@ -188,6 +256,7 @@ int main() {
       case 'S': run_sim(); break;
       case 'W': run_worklist(); break;
       case 'B': run_batch(); break;
+      case 'U': run_upload(); break;
       default: std::fprintf(stderr, "unknown case %s\n", op); return 2;
     }
   }

@@ -41,9 +41,8 @@ def driver(tmp_path_factory):
 
 
 def _run(exe, text):
-    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:halt_on_error=1:abort_on_error=0",
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:halt_on_error=1:abort_on_error=0:verify_asan_link_order=0",
                UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
-    env.pop("LD_PRELOAD", None)
     res = subprocess.run([exe], input=text, capture_output=True, text=True, env=env, timeout=600)
     assert res.returncode == 0 and "Sanitizer" not in res.stderr and "runtime error" not in res.stderr, \
         res.stderr[-4000:]
@@ -175,3 +174,36 @@ def test_work_lists_and_validation_under_sanitizers(driver):
             d = N.AttnDesc(cu32.size - 1, cu32.ctypes.data_as(C.POINTER(C.c_int32)), T, H, D, sc / 1000.0, c)
             n = C.c_size_t()
             assert g == [lib.dcp_varlen_attn_fwd_workspace_size(C.byref(d), C.byref(n))] and g[0] < 0
+
+
+def test_work_list_uploads_under_sanitizers(driver):
+    """The work-list upload plan (the segments the per-call calls and the
+    prepared batch copy to the device): every list and window mask lands at
+    its offset, the bytes between the parts of a segment are zero, nothing
+    outside the segments is written, and a per-call workspace's reserved
+    space is not copied."""
+    rng = random.Random(9)
+    lines, kinds = [], []
+    for _ in range(40):
+        cu = _random_cu(rng)
+        T = int(cu[-1]) + rng.choice([0, 3])
+        H, D, causal = rng.choice([1, 2, 16, 32]), rng.choice([64, 72, 128]), rng.randint(0, 1)
+        for kind in (0, 1, 2):
+            lines.append(" ".join(map(str, ["U", len(cu) - 1, *cu.tolist(), T, H, D, causal, 125, kind])))
+            kinds.append(kind)
+    # the text-pack shape: 75 log-normal documents, 32 heads, causal
+    from paper_2608_07524_amd import inputs as I
+    w = I.text_packs(np.random.default_rng(0), 1)[0]
+    for kind in (0, 1, 2):
+        lines.append(" ".join(map(str, ["U", len(w.lengths), *w.cu_seqlens.tolist(), w.total_tokens, 32, 128, 1, 88,
+                                        kind])))
+        kinds.append(kind)
+    got = _run(driver, "\n".join(lines) + "\n")
+    assert len(got) == len(kinds)
+    for kind, g in zip(kinds, got):
+        status, ok, n_segs, staged, part_bytes, area = g
+        assert status == 0 and ok == 1
+        assert part_bytes <= staged <= part_bytes + (n_segs + 6) * (16 << 10)
+    # the per-call backward of the text pack stages its lists, not the reserved space between them
+    status, ok, n_segs, staged, part_bytes, area = got[-2]
+    assert n_segs >= 2 and staged < area // 4
