@@ -543,6 +543,14 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    props = torch.cuda.get_device_properties(0)
+    dev = P.device_info()
+    # bf16 dense peak from the unit counts: a 32x32x16 product (32,768 flop)
+    # every 32 clocks on each of a CU's four SIMDs
+    dev_peak = dev["compute_units"] * 4 * 1024 * dev["clock_mhz"] * 1e6 / 1e12
+    device = {"name": props.name, "arch": props.gcnArchName, "compute_units": dev["compute_units"],
+              "clock_mhz": dev["clock_mhz"], "bf16_dense_tflops_from_units": dev_peak,
+              "bf16_dense_tflops_used": BF16_PEAK_TFLOPS, "hbm_gbs_used": HBM_PEAK_GBS}
     w, head = measure(torch, P, args.workload, args.steps, args.warmup, args.seed, padded=not args.no_padded)
     line = {
         "metric": METRIC,
@@ -564,6 +572,7 @@ def main():
         "matrix_work": head.get("matrix_work"),
         "host_us_per_call": head.get("host_us_per_call"),
         "padded_baseline": head.get("padded_baseline"),
+        "device": device,
     }
     extras = {}
     for name in [x for x in args.extras.split(",") if x and x != args.workload]:

@@ -234,6 +234,13 @@ int dcp_work_list(const dcp_attn_desc* desc, int32_t pass, int32_t* units, size_
  */
 int dcp_set_kernel_events(void* begin, void* end);
 
+/*
+ * The current device as the runtime reports it, for stating the
+ * denominators of a measurement: compute units and peak engine clock (kHz).
+ * Returns DCP_ERR_HIP when there is no usable gfx950 device.
+ */
+int dcp_device_info(int32_t* compute_units, int32_t* clock_khz);
+
 /* ------------------------------------------------------------------------ */
 /* Per-length cost profile (Sec. 3.5)                                        */
 /* ------------------------------------------------------------------------ */

@@ -113,6 +113,7 @@ def load() -> C.CDLL:
         "dcp_varlen_attn_fwd": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp, sz, vp], C.c_int),
         "dcp_varlen_attn_bwd": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], C.c_int),
         "dcp_set_kernel_events": ([vp, vp], C.c_int),
+        "dcp_device_info": ([C.POINTER(C.c_int32), C.POINTER(C.c_int32)], C.c_int),
         "dcp_varlen_attn_fwd_noalloc": ([C.POINTER(AttnDesc), vp, vp, vp, vp, vp, vp], C.c_int),
         "dcp_batch_create": ([C.POINTER(AttnDesc), C.POINTER(vp)], C.c_int),
         "dcp_batch_workspace_size": ([vp, C.POINTER(sz)], C.c_int),
@@ -343,6 +344,14 @@ class PreparedAttention:
         if getattr(self, "batch", None):
             self.lib.dcp_batch_destroy(self.batch)
             self.batch = None
+
+
+def device_info() -> dict:
+    """Compute units and peak engine clock of the current device (see
+    dcp_device_info)."""
+    cus, khz = C.c_int32(), C.c_int32()
+    _check(load().dcp_device_info(C.byref(cus), C.byref(khz)))
+    return {"compute_units": cus.value, "clock_mhz": khz.value / 1000.0}
 
 
 def set_kernel_events(begin=None, end=None):

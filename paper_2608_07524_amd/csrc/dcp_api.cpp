@@ -225,6 +225,21 @@ extern "C" int dcp_set_kernel_events(void* begin, void* end) {
   return DCP_OK;
 }
 
+extern "C" int dcp_device_info(int32_t* compute_units, int32_t* clock_khz) {
+  clear_error();
+  if (!compute_units || !clock_khz) return fail(DCP_ERR_INVALID, "outputs are null");
+  int dev = -1;
+  int st = check_device(&dev);
+  if (st) return st;
+  int cus = 0, khz = 0;
+  hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&khz, hipDeviceAttributeClockRate, dev);
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "hipDeviceGetAttribute: %s", hipGetErrorString(e));
+  *compute_units = cus;
+  *clock_khz = khz;
+  return DCP_OK;
+}
+
 extern "C" int dcp_varlen_attn_fwd_workspace_size(const dcp_attn_desc* desc, size_t* bytes) {
   clear_error();
   int st = validate_desc(desc);

@@ -82,6 +82,9 @@ def test_pointer_workspace_and_device_errors():
     if not torch.cuda.is_available():
         assert lib.dcp_varlen_attn_fwd(C.byref(d), fake, fake, fake, fake, fake, fake, n.value, None) \
             == N.DCP_ERR_HIP
+        cus, khz = C.c_int32(-1), C.c_int32(-1)
+        assert lib.dcp_device_info(C.byref(cus), C.byref(khz)) == N.DCP_ERR_HIP and cus.value == -1
+    assert lib.dcp_device_info(None, None) == N.DCP_ERR_INVALID
 
 
 def test_profile_validation():

@@ -213,3 +213,12 @@ def test_text_lm_planning_over_1000_packs(torch):
             for f in ("sp_size", "micro_batch", "grad_accum", "recompute_layers", "step_time_ns", "mem_bytes",
                       "idle_ns", "makespan_ns"):
                 assert getattr(got, f) == getattr(ref, f), (g0, f)
+
+
+def test_device_info(torch):
+    """dcp_device_info reports the MI355X's 256 compute units and a plausible
+    engine clock (the denominators bench.py states)."""
+    import paper_2608_07524_amd as P
+    info = P.device_info()
+    assert info["compute_units"] == torch.cuda.get_device_properties(0).multi_processor_count
+    assert info["compute_units"] >= 256 and 1000.0 < info["clock_mhz"] < 4000.0
