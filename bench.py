@@ -389,6 +389,33 @@ def roofline(flop: float, nbytes: float, ms: float, traffic) -> dict:
     return out
 
 
+def mfma_loop_tflops(torch, iters: int = 1000000):
+    """The matrix-core rate of dependent bf16 32x32x16 product chains with
+    nothing else running (one workgroup of 8 wavefronts per CU, two per
+    SIMD, four independent chains each; the probe library's
+    dcp_probe_mfma_rate), about 0.1 s of products timed with HIP events after
+    one untimed launch: the practical ceiling for the kernels' product
+    rates."""
+    import ctypes as C
+    from paper_2608_07524_amd.build import PROBE_LIB
+    probe = C.CDLL(PROBE_LIB)
+    probe.dcp_probe_mfma_rate.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.POINTER(C.c_double)]
+    blocks = torch.cuda.get_device_properties(0).multi_processor_count
+    out = torch.empty(blocks * 512, dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream()
+    flops = C.c_double()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for timed in (False, True):
+        if timed:
+            a.record(s)
+        if probe.dcp_probe_mfma_rate(out.data_ptr(), blocks, iters, 4, C.c_void_p(s.cuda_stream), C.byref(flops)) != 0:
+            raise RuntimeError("matrix-core rate probe failed")
+        if timed:
+            b.record(s)
+    torch.cuda.synchronize()
+    return flops.value / (a.elapsed_time(b) * 1e-3) / 1e12
+
+
 def host_us_per_call(torch, P, w, call, n: int = 5):
     """Host time of one call, averaged over n enqueued calls after one
     untimed call (the device is idle at the start and the calls do not wait
@@ -551,6 +578,7 @@ def main():
     device = {"name": props.name, "arch": props.gcnArchName, "compute_units": dev["compute_units"],
               "clock_mhz": dev["clock_mhz"], "bf16_dense_tflops_from_units": dev_peak,
               "bf16_dense_tflops_used": BF16_PEAK_TFLOPS, "hbm_gbs_used": HBM_PEAK_GBS}
+    device["mfma_loop_tflops"] = mfma_loop_tflops(torch)
     w, head = measure(torch, P, args.workload, args.steps, args.warmup, args.seed, padded=not args.no_padded)
     line = {
         "metric": METRIC,

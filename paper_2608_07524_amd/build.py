@@ -20,7 +20,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdcp.so")
 # measurement probe library (bench.py's counter calibration), not part of libdcp
-PROBE_SOURCES = ["probe/dma_copy.hip"]
+PROBE_SOURCES = ["probe/dma_copy.hip", "probe/mfma_rate.hip"]
 PROBE_LIB = os.path.join(PKG, "libdcp_probe.so")
 
 SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "layer.hip", "dcp_api.cpp", "dcp_error.cpp", "work_list.cpp", "dcp_plan.cpp",
