@@ -137,8 +137,11 @@ int dcp_varlen_attn_bwd(const dcp_attn_desc* desc, const void* dout, const void*
  * dcp_varlen_attn_fwd without a workspace argument.  Its scratch -- the
  * constant chunks, the tile list and the window masks -- lives in a fixed
  * device array of the library, 8 MiB (8,388,608 bytes) per GPU, held until
- * the process ends; the call itself allocates nothing (no hipMalloc, no
- * allocating library routine).  The caller still passes q, k, v, o and lse.
+ * the process ends; the call allocates no device or pinned memory (no
+ * hipMalloc, hipHostMalloc or other allocating HIP or library routine): the
+ * tile list is built in ordinary host memory and copied from there, which
+ * the runtime stages before the call returns.  The caller still passes q,
+ * k, v, o and lse.
  *   Errors: as dcp_varlen_attn_fwd, plus DCP_ERR_WORKSPACE when the batch's
  *   list needs more than 8 MiB (about 520,000 tiles of 256 query rows:
  *   tiles x heads), reported on the host before anything is enqueued.
